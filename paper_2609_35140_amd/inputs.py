@@ -1,0 +1,233 @@
+"""Seeded synthetic workloads for the unified attention path.
+
+This module only draws random numbers and lays them out; it holds none of
+the attention or log-prob arithmetic.  Both the GPU path (through the
+binding) and the CPU oracle consume what it produces, so it is the single
+source of inputs for parity checks.
+
+bf16 tensors are carried on the host as ``numpy.uint16`` bit patterns.
+
+Workload shapes follow the five synthetic configurations of the build
+(tiny, Qwen-style GQA, varlen training pack, GRPO rollout, long context),
+which stand in for the paper's prefill/decode operator workloads
+(Section 6, Q3) and its GSM8K rollouts (Section 6, Q1).
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+BASE_SEED = 42
+
+
+# --------------------------------------------------------------------------
+# random streams
+# --------------------------------------------------------------------------
+def rng(*key: int, seed: int = BASE_SEED) -> np.random.Generator:
+    """A PCG64 generator keyed by ``(seed, *key)``; identical on every host."""
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed, spawn_key=tuple(int(k) for k in key))))
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (round-to-nearest-even) and return the bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
+    out = r.astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        out[nan] = np.uint16(0x7FC0)
+    return out
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Widen bf16 bit patterns to float32 (exact)."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def normal_bf16(shape: Sequence[int], sigma: float, *key: int, seed: int = BASE_SEED) -> np.ndarray:
+    """i.i.d. N(0, sigma^2) samples rounded to bf16, as uint16 bits."""
+    g = rng(*key, seed=seed)
+    x = g.standard_normal(size=tuple(shape), dtype=np.float32) * np.float32(sigma)
+    return f32_to_bf16_bits(x)
+
+
+# --------------------------------------------------------------------------
+# workload descriptions
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class Workload:
+    name: str
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    sigma: float
+    page_size: int
+    prompt_lens: List[int]        # per sequence
+    response_lens: List[int]      # per sequence (decoded tokens); 0 for prefill-only packs
+    vocab: int = 0                # log-prob vocabulary (0: no log-prob leg)
+    logit_sigma: float = 2.0
+    shared_prompt_group: int = 1  # >1: groups of this many sequences share prompt tokens
+
+    @property
+    def seq_lens(self) -> List[int]:
+        return [p + r for p, r in zip(self.prompt_lens, self.response_lens)]
+
+    @property
+    def num_seqs(self) -> int:
+        return len(self.prompt_lens)
+
+    @property
+    def total_tokens(self) -> int:
+        return int(sum(self.seq_lens))
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    def prefill_flop(self) -> float:
+        """Algorithmic causal FLOP: 4*d*Hq per (query, key) pair with key <= query."""
+        d, hq = self.head_dim, self.num_q_heads
+        return float(sum(2.0 * d * hq * L * (L + 1) for L in self.seq_lens))
+
+    def decode_kv_bytes(self) -> float:
+        """Algorithmic decode KV bytes over every response step: K and V once per kv head."""
+        per_tok = 2 * self.num_kv_heads * self.head_dim * 2
+        tot = 0.0
+        for p, r in zip(self.prompt_lens, self.response_lens):
+            # step s decodes token p+s with context p+s+1
+            tot += per_tok * float(sum(range(p + 1, p + r + 1)))
+        return tot
+
+
+def tiny() -> Workload:
+    return Workload("tiny", 2, 1, 64, 1.0, 16, [64], [64])
+
+
+def qwen_gqa() -> Workload:
+    return Workload("qwen_gqa", 32, 8, 128, 0.5, 64, [1024] * 8, [3072] * 8, vocab=151936)
+
+
+def varlen_pack(seed: int = BASE_SEED) -> Workload:
+    g = rng(3, 0, seed=seed)
+    lens = [int(x) for x in g.integers(512, 8192, size=64, endpoint=True)]
+    return Workload("varlen_pack", 40, 8, 128, 1.0, 64, lens, [0] * 64)
+
+
+def grpo_rollout(seed: int = BASE_SEED) -> Workload:
+    g = rng(4, 0, seed=seed)
+    resp = [int(x) for x in g.integers(256, 15360, size=512, endpoint=True)]
+    return Workload("grpo_rollout", 32, 8, 128, 0.5, 64, [1024] * 512, resp, shared_prompt_group=8)
+
+
+def long_context() -> Workload:
+    return Workload("long_context", 64, 8, 128, 0.5, 64, [32768 - 1024] * 8, [1024] * 8, vocab=151936)
+
+
+WORKLOADS = {
+    "tiny": tiny,
+    "qwen_gqa": qwen_gqa,
+    "varlen_pack": varlen_pack,
+    "grpo_rollout": grpo_rollout,
+    "long_context": long_context,
+}
+
+
+def custom(num_q_heads: int, num_kv_heads: int, head_dim: int, seq_lens: Sequence[int],
+           sigma: float = 1.0, page_size: int = 64, prompt_lens: Optional[Sequence[int]] = None,
+           name: str = "custom") -> Workload:
+    seq_lens = [int(s) for s in seq_lens]
+    if prompt_lens is None:
+        prompt_lens = seq_lens
+    prompt_lens = [int(p) for p in prompt_lens]
+    resp = [s - p for s, p in zip(seq_lens, prompt_lens)]
+    return Workload(name, num_q_heads, num_kv_heads, head_dim, sigma, page_size, prompt_lens, resp)
+
+
+# --------------------------------------------------------------------------
+# tensors
+# --------------------------------------------------------------------------
+def cu_seqlens(lens: Sequence[int]) -> np.ndarray:
+    out = np.zeros(len(lens) + 1, dtype=np.int32)
+    out[1:] = np.cumsum(np.asarray(lens, dtype=np.int64)).astype(np.int32)
+    return out
+
+
+def packed_qkv(w: Workload, seed: int = BASE_SEED, tag: int = 0) -> Dict[str, np.ndarray]:
+    """Packed varlen Q [T,Hq,d], K/V [T,Hkv,d] as bf16 bits, plus cu_seqlens.
+
+    Each sequence draws its own tensors from its own stream, so the values of
+    a sequence do not depend on which other sequences share the pack.  With
+    ``shared_prompt_group > 1`` the prompt tokens of each group are identical.
+    """
+    hq, hkv, d = w.num_q_heads, w.num_kv_heads, w.head_dim
+    qs, ks, vs = [], [], []
+    for s, (L, P) in enumerate(zip(w.seq_lens, w.prompt_lens)):
+        grp = s // w.shared_prompt_group
+        if w.shared_prompt_group > 1:
+            pq = normal_bf16((P, hq, d), w.sigma, tag, 1, grp, 0, seed=seed)
+            pk = normal_bf16((P, hkv, d), w.sigma, tag, 1, grp, 1, seed=seed)
+            pv = normal_bf16((P, hkv, d), w.sigma, tag, 1, grp, 2, seed=seed)
+            R = L - P
+            rq = normal_bf16((R, hq, d), w.sigma, tag, 2, s, 0, seed=seed)
+            rk = normal_bf16((R, hkv, d), w.sigma, tag, 2, s, 1, seed=seed)
+            rv = normal_bf16((R, hkv, d), w.sigma, tag, 2, s, 2, seed=seed)
+            qs.append(np.concatenate([pq, rq])); ks.append(np.concatenate([pk, rk])); vs.append(np.concatenate([pv, rv]))
+        else:
+            qs.append(normal_bf16((L, hq, d), w.sigma, tag, 0, s, 0, seed=seed))
+            ks.append(normal_bf16((L, hkv, d), w.sigma, tag, 0, s, 1, seed=seed))
+            vs.append(normal_bf16((L, hkv, d), w.sigma, tag, 0, s, 2, seed=seed))
+    return {
+        "q": np.ascontiguousarray(np.concatenate(qs)),
+        "k": np.ascontiguousarray(np.concatenate(ks)),
+        "v": np.ascontiguousarray(np.concatenate(vs)),
+        "cu_seqlens": cu_seqlens(w.seq_lens),
+    }
+
+
+def paged_layout(seq_lens: Sequence[int], page_size: int, seed: int = BASE_SEED, tag: int = 0,
+                 extra_pages: int = 0, max_pages_per_seq: Optional[int] = None) -> Tuple[np.ndarray, int]:
+    """A block table [B, maxp] (int32) over a shuffled pool of physical pages.
+
+    Logical page j of sequence b lives in physical page ``table[b, j]``; entries
+    past a sequence's last page are -1.  Returns (table, num_physical_pages).
+    """
+    npages = [(int(L) + page_size - 1) // page_size for L in seq_lens]
+    maxp = max(npages) if max_pages_per_seq is None else int(max_pages_per_seq)
+    total = int(sum(npages)) + int(extra_pages)
+    perm = rng(9, tag, seed=seed).permutation(total).astype(np.int32)
+    table = np.full((len(seq_lens), maxp), -1, dtype=np.int32)
+    pos = 0
+    for b, n in enumerate(npages):
+        table[b, :n] = perm[pos:pos + n]
+        pos += n
+    return table, total
+
+
+def scatter_to_pages(x: np.ndarray, cu: np.ndarray, table: np.ndarray, num_pages: int, page_size: int,
+                     fill_bits: int = 0x7FC0) -> np.ndarray:
+    """Lay packed [T,H,d] rows into a paged cache [P,H,page,d] (HND).
+
+    Slots that hold no token are filled with ``fill_bits`` (a bf16 NaN by
+    default) so that any read of an unwritten slot shows up in the results.
+    """
+    T, H, d = x.shape
+    pages = np.full((num_pages, H, page_size, d), fill_bits, dtype=np.uint16)
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        for j in range(0, hi - lo, page_size):
+            n = min(page_size, hi - lo - j)
+            p = int(table[b, j // page_size])
+            pages[p, :, :n, :] = np.transpose(x[lo + j:lo + j + n], (1, 0, 2))
+    return pages
+
+
+def logits_bf16(rows: int, vocab: int, sigma: float, seed: int = BASE_SEED, tag: int = 0) -> np.ndarray:
+    return normal_bf16((rows, vocab), sigma, 7, tag, seed=seed)
+
+
+def targets(rows: int, vocab: int, seed: int = BASE_SEED, tag: int = 0) -> np.ndarray:
+    return rng(8, tag, seed=seed).integers(0, vocab, size=rows).astype(np.int32)
