@@ -1,0 +1,160 @@
+/*
+ * uattn -- unified, batch-invariant causal GQA attention for MI355X (gfx950).
+ *
+ * C ABI of libuattn.so.  Two entry points compute the same attention for
+ * the two execution regimes the paper couples (Section 1 and Section 4.1):
+ *
+ *   uattn_prefill  -- the full-sequence entry point, used by the policy
+ *                     update over whole prompt+response trajectories and by
+ *                     rollout prefill over prompts;
+ *   uattn_decode   -- the token-wise decode entry point, one new query per
+ *                     sequence against a paged KV cache.
+ *
+ * For the same token, query, causal KV prefix and weights, the two return
+ * bit-identical outputs (the operator-level form of Eq. (1), Section 3.2),
+ * independent of batch size, batch order, max_seqlen and how decode splits
+ * its work.  uattn_logprob is the per-token log-softmax gather whose equality
+ * across the two regimes makes the reuse ratio exp(l_upd - l_roll) exactly 1
+ * (Section 3.1).
+ *
+ * Conventions shared by every call:
+ *   - every pointer argument is a DEVICE pointer unless stated otherwise;
+ *   - bf16 tensors are raw 16-bit bfloat16 values, row-major, contiguous;
+ *   - the caller owns every buffer; the library never allocates, frees or
+ *     synchronizes; each call enqueues kernels on `stream` (a hipStream_t,
+ *     NULL for the default stream) and returns;
+ *   - outputs must not alias inputs;
+ *   - integer data that lives on the device (cu_seqlens, seqlens,
+ *     block_table, targets) is trusted: it is not read by the host.  Setting
+ *     the environment variable UATTN_VALIDATE=1 makes the host copy it back
+ *     (synchronously) and check it before launching, for debugging;
+ *   - errors are reported by the return code only; nothing is printed and
+ *     nothing aborts.  On any non-OK code no kernel was launched, except
+ *     UATTN_ELAUNCH, which reports a failure of the launch itself.
+ */
+#ifndef UATTN_H
+#define UATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define UATTN_ABI_VERSION 1
+
+typedef enum {
+  UATTN_OK = 0,
+  UATTN_EINVAL = 1,       /* null pointer, negative or inconsistent sizes, Hq % Hkv != 0, bad scale */
+  UATTN_EUNSUPPORTED = 2, /* head_dim not 64/128, page_size not a power of two >= 16, group > 32 */
+  UATTN_EWORKSPACE = 3,   /* decode workspace missing or smaller than uattn_decode_workspace_bytes() */
+  UATTN_ELAUNCH = 4       /* the HIP runtime rejected a kernel launch */
+} uattn_status;
+
+/* Version of this ABI (UATTN_ABI_VERSION). */
+int32_t uattn_abi_version(void);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char* uattn_status_string(int32_t status);
+
+/*
+ * Full-sequence causal attention over a packed varlen batch (Section 3.2:
+ * scores Q K^T, weights P = softmax, output P V; Section 4.1: one invocation
+ * processes a whole trajectory under causal masking).
+ *
+ *   q          [total_tokens, num_q_heads, head_dim]  bf16
+ *   k, v       [total_tokens, num_kv_heads, head_dim] bf16
+ *   cu_seqlens [num_seqs + 1] int32, cu_seqlens[0] = 0, non-decreasing,
+ *              cu_seqlens[num_seqs] = total_tokens; sequence s holds packed
+ *              rows cu_seqlens[s] .. cu_seqlens[s+1]-1 (offsets outside
+ *              [0, total_tokens] are clamped, so a bad table cannot make the
+ *              kernel read or write outside the tensors)
+ *   max_seqlen host int >= every sequence length (sizes the launch grid
+ *              only; results do not depend on it)
+ *   softmax_scale  finite, > 0 (usually 1/sqrt(head_dim))
+ *   out        [total_tokens, num_q_heads, head_dim] bf16 (written)
+ *   lse        [total_tokens, num_q_heads] fp32 natural-log sum of
+ *              exp(scale * score) per row, or NULL
+ *
+ * Row i of a sequence attends keys 0..i of the same sequence (positions
+ * are sequence-relative).  Query head h reads kv head h / (Hq / Hkv).
+ * Empty sequences are allowed.  head_dim must be 64 or 128.
+ */
+uattn_status uattn_prefill(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                           int32_t num_seqs, int32_t total_tokens, int32_t max_seqlen,
+                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                           float softmax_scale, void* out, float* lse, void* stream);
+
+/*
+ * Bytes of device workspace uattn_decode needs for these sizes (the fp32
+ * partials of the positional split; 0 when no entry can span two chunks).
+ * Pure host arithmetic; returns 0 for invalid sizes.
+ */
+size_t uattn_decode_workspace_bytes(int32_t batch, int32_t max_seqlen, int32_t num_q_heads, int32_t head_dim);
+
+/*
+ * Token-wise decode against a paged KV cache (Section 3.1: the cache
+ * represents the prefix x_i; Section 3.2: one new query at a time).
+ *
+ *   q            [batch, num_q_heads, head_dim] bf16; entry b's query is the
+ *                token at position seqlens[b]-1
+ *   k_pages,
+ *   v_pages      [num_pages, num_kv_heads, page_size, head_dim] bf16 (HND);
+ *                logical position j of entry b lives in physical page
+ *                block_table[b * max_pages_per_seq + j / page_size], slot
+ *                j % page_size.  The current token's K/V must already be
+ *                written.  Slots at positions >= seqlens[b] are never read,
+ *                nor are block_table entries past the last used page.
+ *   num_pages    number of physical pages P; a block_table entry outside
+ *                [0, P) is never dereferenced (its keys read as zeros)
+ *   block_table  [batch, max_pages_per_seq] int32
+ *   seqlens      [batch] int32, 1 <= seqlens[b] <= max_seqlen (includes the
+ *                current token); values outside that range are clamped to
+ *                it (an entry with seqlens[b] < 1 is left unwritten)
+ *   max_seqlen   host int >= every seqlens[b] (sizes grid and workspace only)
+ *   out          [batch, num_q_heads, head_dim] bf16 (written)
+ *   lse          [batch, num_q_heads] fp32, or NULL
+ *   workspace    device scratch of at least
+ *                uattn_decode_workspace_bytes(batch, max_seqlen, Hq, d) bytes
+ *                (may be NULL when that is 0); contents need no initialization
+ *                and are overwritten.  Calls that share a workspace must be
+ *                ordered on one stream.
+ *
+ * Keys are split into fixed 256-position chunks; each chunk's partial
+ * softmax state is folded in ascending chunk order, so results do not depend
+ * on the batch, its order or the split.  (num_q_heads / num_kv_heads) <= 32.
+ */
+uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_pages,
+                          const int32_t* block_table, const int32_t* seqlens, int32_t batch,
+                          int32_t max_pages_per_seq, int32_t page_size, int32_t num_pages, int32_t max_seqlen,
+                          int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                          float softmax_scale, void* out, float* lse,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Per-token log-probability of the recorded token (Section 3.1: the same
+ * deterministic logit processing and normalization in both regimes):
+ *
+ *   logp[t] = x_t[targets[t]] - log sum_v exp(x_t[v]),  x_t = logits[t] * inv_temperature
+ *
+ *   logits       [num_rows, row_stride] bf16, the first `vocab` entries of
+ *                each row are used; the pointer must be 16-byte aligned and
+ *                row_stride a multiple of 8 (elements)
+ *   targets      [num_rows] int32 in [0, vocab); a row whose target is
+ *                outside that range gets NaN
+ *   inv_temperature  finite, > 0
+ *   logp         [num_rows] fp32 (written)
+ *
+ * Each row is reduced by one workgroup in a fixed order that depends only on
+ * vocab, so a row's result is bit-identical whatever num_rows or its position.
+ */
+uattn_status uattn_logprob(const void* logits, int64_t row_stride, const int32_t* targets,
+                           int32_t num_rows, int32_t vocab, float inv_temperature, float* logp,
+                           void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UATTN_H */

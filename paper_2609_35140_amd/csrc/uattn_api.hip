@@ -1,0 +1,183 @@
+// extern "C" boundary of libuattn: argument validation, grid sizing and
+// launch on the caller's stream.  No allocation, no synchronization (except
+// the opt-in UATTN_VALIDATE debug copies), no global mutable state.
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "../../include/uattn.h"
+#include "uattn_internal.h"
+#include "uattn_numerics.h"
+
+namespace {
+
+using uattn::kChunkKeys;
+
+constexpr double kLog2e = 1.4426950408889634;
+
+bool scale_ok(float s) { return s > 0.f && s < __builtin_inff(); }
+
+bool validate_env() {
+  const char* e = getenv("UATTN_VALIDATE");
+  return e != nullptr && e[0] != '\0' && e[0] != '0';
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// fp32(scale * log2(e)), the one constant both attention paths fold into exp2.
+float exp2_scale(float softmax_scale) { return static_cast<float>(static_cast<double>(softmax_scale) * kLog2e); }
+
+template <class T>
+bool copy_back(std::vector<T>& host, const T* dev, size_t n) {
+  host.resize(n);
+  if (n == 0) return true;
+  return hipMemcpy(host.data(), dev, n * sizeof(T), hipMemcpyDeviceToHost) == hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t uattn_abi_version(void) { return UATTN_ABI_VERSION; }
+
+const char* uattn_status_string(int32_t status) {
+  switch (status) {
+    case UATTN_OK: return "UATTN_OK";
+    case UATTN_EINVAL: return "UATTN_EINVAL: invalid argument";
+    case UATTN_EUNSUPPORTED: return "UATTN_EUNSUPPORTED: unsupported shape";
+    case UATTN_EWORKSPACE: return "UATTN_EWORKSPACE: workspace missing or too small";
+    case UATTN_ELAUNCH: return "UATTN_ELAUNCH: kernel launch failed";
+    default: return "UATTN_UNKNOWN_STATUS";
+  }
+}
+
+uattn_status uattn_prefill(const void* q, const void* k, const void* v, const int32_t* cu_seqlens, int32_t num_seqs,
+                           int32_t total_tokens, int32_t max_seqlen, int32_t num_q_heads, int32_t num_kv_heads,
+                           int32_t head_dim, float softmax_scale, void* out, float* lse, void* stream) {
+  if (num_seqs < 0 || total_tokens < 0 || max_seqlen < 0 || num_q_heads <= 0 || num_kv_heads <= 0)
+    return UATTN_EINVAL;
+  if (num_q_heads % num_kv_heads != 0 || !scale_ok(softmax_scale)) return UATTN_EINVAL;
+  if (head_dim != 64 && head_dim != 128) return UATTN_EUNSUPPORTED;
+  if (num_seqs > 65535) return UATTN_EUNSUPPORTED;
+  if (num_seqs == 0 || total_tokens == 0 || max_seqlen == 0) return UATTN_OK;
+  if (!q || !k || !v || !cu_seqlens || !out) return UATTN_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return UATTN_EINVAL;
+  if ((static_cast<int64_t>(max_seqlen) + 127) / 128 > 65535) return UATTN_EUNSUPPORTED;
+  if (validate_env()) {
+    std::vector<int32_t> cu;
+    if (!copy_back(cu, cu_seqlens, static_cast<size_t>(num_seqs) + 1)) return UATTN_EINVAL;
+    if (cu[0] != 0 || cu[num_seqs] != total_tokens) return UATTN_EINVAL;
+    for (int32_t s = 0; s < num_seqs; ++s) {
+      const int32_t len = cu[s + 1] - cu[s];
+      if (len < 0 || len > max_seqlen) return UATTN_EINVAL;
+    }
+  }
+  uattn::PrefillLaunch a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.cu_seqlens = cu_seqlens;
+  a.out = out;
+  a.lse = lse;
+  a.num_seqs = num_seqs;
+  a.total_tokens = total_tokens;
+  a.max_seqlen = max_seqlen;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.c = exp2_scale(softmax_scale);
+  return uattn::launch_prefill(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
+}
+
+size_t uattn_decode_workspace_bytes(int32_t batch, int32_t max_seqlen, int32_t num_q_heads, int32_t head_dim) {
+  if (batch <= 0 || max_seqlen <= 0 || num_q_heads <= 0 || head_dim <= 0) return 0;
+  const int64_t nchunk = (static_cast<int64_t>(max_seqlen) + kChunkKeys - 1) / kChunkKeys;
+  if (nchunk <= 1) return 0;
+  return uattn::decode_ws_acc_bytes(batch, nchunk, num_q_heads, head_dim) +
+         uattn::decode_ws_ml_bytes(batch, nchunk, num_q_heads);
+}
+
+uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+                          const int32_t* seqlens, int32_t batch, int32_t max_pages_per_seq, int32_t page_size,
+                          int32_t num_pages, int32_t max_seqlen, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                          float softmax_scale, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  if (batch < 0 || max_pages_per_seq < 0 || max_seqlen < 0 || num_pages < 0 || num_q_heads <= 0 ||
+      num_kv_heads <= 0)
+    return UATTN_EINVAL;
+  if (num_q_heads % num_kv_heads != 0 || !scale_ok(softmax_scale)) return UATTN_EINVAL;
+  if (head_dim != 64 && head_dim != 128) return UATTN_EUNSUPPORTED;
+  if (page_size < 16 || (page_size & (page_size - 1)) != 0) return UATTN_EUNSUPPORTED;
+  if (num_q_heads / num_kv_heads > uattn::kQCols) return UATTN_EUNSUPPORTED;
+  if (batch > 65535 || num_kv_heads > 65535) return UATTN_EUNSUPPORTED;
+  if (batch == 0) return UATTN_OK;
+  if (max_seqlen == 0 || num_pages == 0) return UATTN_EINVAL;  // every entry holds at least its own token
+  if (static_cast<int64_t>(max_pages_per_seq) * page_size < max_seqlen) return UATTN_EINVAL;
+  if (!q || !k_pages || !v_pages || !block_table || !seqlens || !out) return UATTN_EINVAL;
+  if (!aligned16(q) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned16(out)) return UATTN_EINVAL;
+  const size_t need = uattn_decode_workspace_bytes(batch, max_seqlen, num_q_heads, head_dim);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))) return UATTN_EWORKSPACE;
+  const int64_t nchunk = (static_cast<int64_t>(max_seqlen) + kChunkKeys - 1) / kChunkKeys;
+  if (validate_env()) {
+    std::vector<int32_t> sl, bt;
+    if (!copy_back(sl, seqlens, static_cast<size_t>(batch))) return UATTN_EINVAL;
+    if (!copy_back(bt, block_table, static_cast<size_t>(batch) * max_pages_per_seq)) return UATTN_EINVAL;
+    for (int32_t b = 0; b < batch; ++b) {
+      if (sl[b] < 1 || sl[b] > max_seqlen) return UATTN_EINVAL;
+      const int32_t used = (sl[b] + page_size - 1) / page_size;
+      for (int32_t j = 0; j < used; ++j)
+        if (bt[static_cast<size_t>(b) * max_pages_per_seq + j] < 0 ||
+            bt[static_cast<size_t>(b) * max_pages_per_seq + j] >= num_pages)
+          return UATTN_EINVAL;
+    }
+  }
+  uattn::DecodeLaunch a;
+  a.q = q;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.block_table = block_table;
+  a.seqlens = seqlens;
+  a.out = out;
+  a.lse = lse;
+  a.ws_acc = static_cast<float*>(workspace);
+  a.ws_ml = need > 0 ? reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                                uattn::decode_ws_acc_bytes(batch, nchunk, num_q_heads, head_dim))
+                     : nullptr;
+  a.batch = batch;
+  a.max_pages_per_seq = max_pages_per_seq;
+  a.page_size = page_size;
+  a.num_pages = num_pages;
+  a.max_seqlen = max_seqlen;
+  a.nchunk_max = static_cast<int32_t>(nchunk);
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.c = exp2_scale(softmax_scale);
+  return uattn::launch_decode(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
+}
+
+uattn_status uattn_logprob(const void* logits, int64_t row_stride, const int32_t* targets, int32_t num_rows,
+                           int32_t vocab, float inv_temperature, float* logp, void* stream) {
+  if (num_rows < 0 || vocab <= 0 || row_stride < vocab || !scale_ok(inv_temperature)) return UATTN_EINVAL;
+  if (num_rows == 0) return UATTN_OK;
+  if (!logits || !targets || !logp) return UATTN_EINVAL;
+  if (!aligned16(logits) || (row_stride % 8) != 0) return UATTN_EINVAL;
+  if (validate_env()) {
+    std::vector<int32_t> tg;
+    if (!copy_back(tg, targets, static_cast<size_t>(num_rows))) return UATTN_EINVAL;
+    for (int32_t t : tg)
+      if (t < 0 || t >= vocab) return UATTN_EINVAL;
+  }
+  uattn::LogprobLaunch a;
+  a.logits = logits;
+  a.row_stride = row_stride;
+  a.targets = targets;
+  a.logp = logp;
+  a.num_rows = num_rows;
+  a.vocab = vocab;
+  a.inv_temperature = inv_temperature;
+  return uattn::launch_logprob(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
+}
+
+}  // extern "C"

@@ -1,0 +1,67 @@
+// Internal launcher interface between the C-ABI layer and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace uattn {
+
+struct PrefillLaunch {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* cu_seqlens;
+  void* out;
+  float* lse;
+  int32_t num_seqs;
+  int32_t total_tokens;
+  int32_t max_seqlen;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  float c;  // fp32(scale * log2(e))
+};
+
+struct DecodeLaunch {
+  const void* q;
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* block_table;
+  const int32_t* seqlens;
+  void* out;
+  float* lse;
+  float* ws_acc;  // [batch][Hq][nchunk_max][head_dim]
+  float* ws_ml;   // [batch][Hq][nchunk_max][2]
+  int32_t batch;
+  int32_t max_pages_per_seq;
+  int32_t page_size;
+  int32_t num_pages;
+  int32_t max_seqlen;
+  int32_t nchunk_max;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  float c;
+};
+
+struct LogprobLaunch {
+  const void* logits;
+  int64_t row_stride;
+  const int32_t* targets;
+  float* logp;
+  int32_t num_rows;
+  int32_t vocab;
+  float inv_temperature;
+};
+
+// Each returns hipSuccess or the launch error.
+hipError_t launch_prefill(const PrefillLaunch& a, hipStream_t stream);
+hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream);
+hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t stream);
+
+// Decode workspace split (bytes of the acc part; the m/l part follows it).
+size_t decode_ws_acc_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads, int64_t head_dim);
+size_t decode_ws_ml_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads);
+
+}  // namespace uattn

@@ -1,0 +1,189 @@
+"""Python binding for libuattn.so (argument marshalling only).
+
+Every function here checks shapes/dtypes, takes device pointers from torch
+tensors and calls the C ABI declared in ``include/uattn.h`` on the current
+torch stream.  All arithmetic runs in the HIP kernels; there is no CPU or
+PyTorch fallback -- if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Tuple
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libuattn.so")
+
+UATTN_OK = 0
+TILE_KEYS = 64
+CHUNK_KEYS = 256
+
+_lib = None
+
+
+class UattnError(RuntimeError):
+    pass
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise UattnError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_35140_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    c_i32, c_i64, c_f, c_p, c_sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+    lib.uattn_abi_version.restype = c_i32
+    lib.uattn_abi_version.argtypes = []
+    lib.uattn_status_string.restype = ctypes.c_char_p
+    lib.uattn_status_string.argtypes = [c_i32]
+    lib.uattn_prefill.restype = c_i32
+    lib.uattn_prefill.argtypes = [c_p, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_f, c_p, c_p, c_p]
+    lib.uattn_decode_workspace_bytes.restype = c_sz
+    lib.uattn_decode_workspace_bytes.argtypes = [c_i32, c_i32, c_i32, c_i32]
+    lib.uattn_decode.restype = c_i32
+    lib.uattn_decode.argtypes = [c_p, c_p, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_f,
+                                 c_p, c_p, c_p, c_sz, c_p]
+    lib.uattn_logprob.restype = c_i32
+    lib.uattn_logprob.argtypes = [c_p, c_i64, c_p, c_i32, c_i32, c_f, c_p, c_p]
+    _lib = lib
+    return lib
+
+
+def lib():
+    """The loaded ctypes library (raises if it is not built)."""
+    return _load()
+
+
+def abi_version() -> int:
+    return int(_load().uattn_abi_version())
+
+
+def status_string(code: int) -> str:
+    return _load().uattn_status_string(int(code)).decode()
+
+
+def _check(code: int):
+    if code != UATTN_OK:
+        raise UattnError(status_string(code))
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _bf16_cuda(t, name):
+    import torch
+    _need(t.is_cuda, f"{name} must be a GPU tensor")
+    _need(t.dtype == torch.bfloat16, f"{name} must be bfloat16")
+    _need(t.is_contiguous(), f"{name} must be contiguous")
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)
+
+
+def prefill(q, k, v, cu_seqlens, max_seqlen: int, softmax_scale: Optional[float] = None, out=None,
+            return_lse: bool = False, lse=None, stream=None):
+    """Full-sequence causal attention (uattn_prefill).
+
+    q [T,Hq,d], k/v [T,Hkv,d] bf16 CUDA; cu_seqlens int32 CUDA [B+1].
+    Returns out [T,Hq,d] (and lse [T,Hq] fp32 if requested).
+    """
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _bf16_cuda(t, name)
+    _need(q.dim() == 3 and k.dim() == 3 and v.dim() == 3, "q/k/v must be [T, H, d]")
+    T, hq, d = q.shape
+    _need(k.shape == v.shape and k.shape[0] == T and k.shape[2] == d, "k/v shape mismatch")
+    _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.is_cuda and cu_seqlens.is_contiguous(),
+          "cu_seqlens must be contiguous int32 on the GPU")
+    if softmax_scale is None:
+        softmax_scale = default_scale(d)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _bf16_cuda(out, "out")
+        _need(out.shape == q.shape, "out shape")
+    if return_lse and lse is None:
+        lse = torch.empty((T, hq), dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse.dtype == torch.float32 and lse.is_contiguous() and lse.shape == (T, hq), "lse must be [T,Hq] fp32")
+    _check(_load().uattn_prefill(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), cu_seqlens.numel() - 1, T,
+                                 int(max_seqlen), hq, k.shape[1], d, float(softmax_scale), _ptr(out), _ptr(lse),
+                                 _stream(stream)))
+    return (out, lse) if lse is not None else out
+
+
+def decode_workspace_bytes(batch: int, max_seqlen: int, num_q_heads: int, head_dim: int) -> int:
+    return int(_load().uattn_decode_workspace_bytes(batch, max_seqlen, num_q_heads, head_dim))
+
+
+def decode(q, k_pages, v_pages, block_table, seqlens, max_seqlen: int, softmax_scale: Optional[float] = None,
+           out=None, return_lse: bool = False, lse=None, workspace=None, stream=None):
+    """Token-wise paged decode (uattn_decode).
+
+    q [B,Hq,d]; k_pages/v_pages [P,Hkv,page,d] bf16 CUDA; block_table [B,maxp]
+    int32; seqlens [B] int32 (context length including the current token).
+    ``workspace`` is a uint8 CUDA tensor; allocated here when not given.
+    """
+    import torch
+    for name, t in (("q", q), ("k_pages", k_pages), ("v_pages", v_pages)):
+        _bf16_cuda(t, name)
+    _need(q.dim() == 3 and k_pages.dim() == 4 and v_pages.shape == k_pages.shape, "shapes: q [B,Hq,d], pages [P,Hkv,page,d]")
+    B, hq, d = q.shape
+    _, hkv, page, d2 = k_pages.shape
+    _need(d2 == d, "head_dim mismatch")
+    for name, t in (("block_table", block_table), ("seqlens", seqlens)):
+        _need(t.dtype == torch.int32 and t.is_cuda and t.is_contiguous(), f"{name} must be contiguous int32 on the GPU")
+    _need(block_table.dim() == 2 and block_table.shape[0] == B and seqlens.shape == (B,), "block_table/seqlens shape")
+    if softmax_scale is None:
+        softmax_scale = default_scale(d)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _bf16_cuda(out, "out")
+        _need(out.shape == q.shape, "out shape")
+    if return_lse and lse is None:
+        lse = torch.empty((B, hq), dtype=torch.float32, device=q.device)
+    need = decode_workspace_bytes(B, int(max_seqlen), hq, d) if B > 0 else 0
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_load().uattn_decode(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table), _ptr(seqlens), B,
+                                block_table.shape[1], page, k_pages.shape[0], int(max_seqlen), hq, hkv, d, float(softmax_scale),
+                                _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream)))
+    return (out, lse) if lse is not None else out
+
+
+def logprob(logits, targets, inv_temperature: float = 1.0, out=None, stream=None):
+    """Per-token log-probability (uattn_logprob). logits [T,V] bf16 (row stride may exceed V)."""
+    import torch
+    _need(logits.is_cuda and logits.dtype == torch.bfloat16 and logits.dim() == 2, "logits must be [T,V] bf16 on the GPU")
+    _need(logits.stride(1) == 1, "logits rows must be contiguous")
+    T, V = logits.shape
+    _need(targets.dtype == torch.int32 and targets.is_cuda and targets.shape == (T,) and targets.is_contiguous(),
+          "targets must be [T] int32 on the GPU")
+    if out is None:
+        out = torch.empty(T, dtype=torch.float32, device=logits.device)
+    _check(_load().uattn_logprob(_ptr(logits), logits.stride(0), _ptr(targets), T, V, float(inv_temperature),
+                                 _ptr(out), _stream(stream)))
+    return out
+
+
+def raw_call(name: str, *args) -> int:
+    """Call a C entry point with raw arguments (for error-path tests)."""
+    return int(getattr(_load(), name)(*args))

@@ -1,0 +1,117 @@
+"""The C-ABI library on the host: it loads, exports every declared entry
+point, and its argument checks reject bad calls before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "uattn.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(uattn_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_35140_amd import uattn
+    if not os.path.exists(uattn.LIB_PATH):
+        from paper_2609_35140_amd import build
+        build.build()
+    return uattn.lib()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ["uattn_prefill", "uattn_decode", "uattn_decode_workspace_bytes", "uattn_logprob",
+              "uattn_status_string", "uattn_abi_version"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+    # no C++ mangling on the boundary
+    so = ctypes.CDLL(os.path.join(ROOT, "paper_2609_35140_amd", "libuattn.so"))
+    for n in declared_functions():
+        getattr(so, n)
+
+
+def test_abi_version_and_status_strings(lib):
+    from paper_2609_35140_amd import uattn
+    assert uattn.abi_version() == 1
+    assert uattn.status_string(0) == "UATTN_OK"
+    for code in range(1, 5):
+        assert uattn.status_string(code).startswith("UATTN_E")
+    assert "UNKNOWN" in uattn.status_string(99)
+
+
+def test_workspace_bytes(lib):
+    from paper_2609_35140_amd import uattn
+    assert uattn.decode_workspace_bytes(8, 256, 32, 128) == 0        # one chunk: no partials
+    assert uattn.decode_workspace_bytes(8, 257, 32, 128) == 8 * 32 * 2 * (128 + 2) * 4
+    assert uattn.decode_workspace_bytes(8, 4096, 32, 128) == 8 * 32 * 16 * 130 * 4
+    assert uattn.decode_workspace_bytes(0, 4096, 32, 128) == 0
+    assert uattn.decode_workspace_bytes(1, -5, 32, 128) == 0
+
+
+P = ctypes.c_void_p
+
+
+def _prefill(lib, **kw):
+    a = dict(q=P(16), k=P(16), v=P(16), cu=P(16), ns=1, T=4, maxs=4, hq=4, hkv=2, d=128, scale=0.1,
+             out=P(32), lse=None, stream=None)
+    a.update(kw)
+    return lib.uattn_prefill(a["q"], a["k"], a["v"], a["cu"], a["ns"], a["T"], a["maxs"], a["hq"], a["hkv"], a["d"],
+                             a["scale"], a["out"], a["lse"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hq=3, hkv=2), 1), (dict(hkv=0), 1), (dict(ns=-1), 1), (dict(scale=0.0), 1),
+    (dict(scale=float("inf")), 1), (dict(scale=float("nan")), 1), (dict(scale=-1.0), 1),
+    (dict(d=96), 2), (dict(d=256), 2), (dict(q=None), 1), (dict(out=None), 1), (dict(q=P(18)), 1),
+    (dict(ns=0), 0), (dict(T=0), 0), (dict(maxs=0), 0),
+])
+def test_prefill_argument_checks(lib, kw, code):
+    assert _prefill(lib, **kw) == code
+
+
+def _decode(lib, **kw):
+    a = dict(q=P(16), kp=P(16), vp=P(16), bt=P(16), sl=P(16), B=2, maxp=4, page=16, npages=10, maxs=64, hq=8, hkv=2, d=128,
+             scale=0.1, out=P(32), lse=None, ws=None, wsb=0, stream=None)
+    a.update(kw)
+    return lib.uattn_decode(a["q"], a["kp"], a["vp"], a["bt"], a["sl"], a["B"], a["maxp"], a["page"], a["npages"], a["maxs"],
+                            a["hq"], a["hkv"], a["d"], a["scale"], a["out"], a["lse"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hq=9), 1), (dict(page=24), 2), (dict(page=8), 2), (dict(d=80), 2), (dict(hq=66, hkv=2), 2),
+    (dict(maxp=3), 1), (dict(maxs=0), 1), (dict(bt=None), 1), (dict(scale=0.0), 1),
+    (dict(npages=0), 1), (dict(npages=-1), 1), (dict(maxs=300, maxp=19), 3), (dict(maxs=300, maxp=19, ws=P(64), wsb=100), 3), (dict(B=0), 0),
+])
+def test_decode_argument_checks(lib, kw, code):
+    assert _decode(lib, **kw) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((P(16), 8, P(16), 4, 0, 1.0, P(16), None), 1),       # vocab 0
+    ((P(16), 4, P(16), 4, 8, 1.0, P(16), None), 1),       # stride < vocab
+    ((P(16), 12, P(16), 4, 8, 1.0, P(16), None), 1),      # stride not a multiple of 8
+    ((P(18), 8, P(16), 4, 8, 1.0, P(16), None), 1),       # misaligned logits
+    ((P(16), 8, P(16), 4, 8, 0.0, P(16), None), 1),       # temperature
+    ((P(16), 8, P(16), 0, 8, 1.0, P(16), None), 0),       # no rows
+])
+def test_logprob_argument_checks(lib, args, code):
+    assert lib.uattn_logprob(*args) == code
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    from paper_2609_35140_amd import uattn
+    monkeypatch.setattr(uattn, "_lib", None)
+    monkeypatch.setattr(uattn, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(uattn.UattnError):
+        uattn.abi_version()

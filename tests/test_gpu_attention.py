@@ -1,0 +1,243 @@
+"""GPU parity and bitwise-consistency tests of the unified attention path.
+
+Parity: GPU outputs vs the fp64 oracle under the gate (mean |err| <= 5e-4,
+per element |err| <= 4e-3 + 2^-8 |ref|).  Consistency (Eq. (1) at operator
+level, Section 3.2): every decoded row equals the full-sequence row at the
+same position bit for bit, under varied batch mixes, orders and splits.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_35140_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+gu = pytest.importorskip("gpu_util")
+
+
+@pytest.fixture(scope="module")
+def ua():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_35140_amd import uattn
+    uattn.lib()
+    return uattn
+
+
+def _prefill(ua, pk, lse=True):
+    out, l = ua.prefill(pk.q, pk.k, pk.v, pk.cu_dev, pk.max_seqlen, return_lse=True)
+    return out, l
+
+
+SMALL = [
+    ("tiny_s1", lambda: inputs.tiny(), 1),
+    ("tiny_s42", lambda: inputs.tiny(), 42),
+    ("tiny_s1023", lambda: inputs.tiny(), 1023),
+    ("d128_g4_ragged", lambda: inputs.custom(8, 2, 128, [1, 63, 64, 65, 300, 700], sigma=1.0, page_size=64), 42),
+    ("d64_g5_ragged", lambda: inputs.custom(10, 2, 64, [31, 257, 513, 130], sigma=1.0, page_size=16), 42),
+    ("d128_g8", lambda: inputs.custom(16, 2, 128, [1000, 257], sigma=0.5, page_size=64), 42),
+    ("d128_mha", lambda: inputs.custom(3, 3, 128, [200, 77], sigma=1.0, page_size=32), 42),
+    ("d64_g32", lambda: inputs.custom(32, 1, 64, [300], sigma=1.0, page_size=128), 42),
+]
+
+
+@pytest.mark.parametrize("name,mk,seed", SMALL, ids=[s[0] for s in SMALL])
+def test_prefill_matches_oracle(ua, name, mk, seed):
+    w = mk()
+    pk = gu.Pack(w, seed=seed)
+    out, lse = _prefill(ua, pk)
+    o64, lse64 = oracle.causal_attention_fp64(pk.host["q"], pk.host["k"], pk.host["v"], pk.cu)
+    rep = oracle.parity_report(gu.host_f64(out), o64)
+    print(name, rep, flush=True)
+    assert rep["pass"], rep
+    lg = lse.cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(lg - lse64)) < 2e-4, np.max(np.abs(lg - lse64))
+
+
+@pytest.mark.parametrize("name,mk,seed", SMALL, ids=[s[0] for s in SMALL])
+def test_decode_every_position_bitwise_equals_prefill(ua, name, mk, seed):
+    """Decode of every (sequence, position) in one batched call equals the
+    full-sequence output rows bit for bit, lse included."""
+    w = mk()
+    pk = gu.Pack(w, seed=seed)
+    out, lse = _prefill(ua, pk)
+    entries = [(s, p) for s, L in enumerate(w.seq_lens) for p in range(L)]
+    q, table, seqlens, maxs, tok = pk.decode_rows(entries)
+    dout, dlse = ua.decode(q, pk.kp, pk.vp, table, seqlens, maxs, return_lse=True)
+    a = gu.host_bits(dout)
+    b = gu.host_bits(out)[tok]
+    eq = gu.rows_equal_bits(a, b)
+    print(name, "bitwise rows", eq.mean(), flush=True)
+    assert eq.all(), f"{(~eq).sum()} of {eq.size} rows differ"
+    assert np.array_equal(dlse.cpu().numpy().view(np.uint32), lse.cpu().numpy()[tok].view(np.uint32))
+    # and the decode result itself meets the oracle gate
+    o64, _ = oracle.paged_decode_fp64(pk.host["q"][tok], pk.kp_host, pk.vp_host, pk.table[[s for s, _ in entries]],
+                                      [p + 1 for _, p in entries])
+    assert oracle.parity_report(gu.host_f64(dout), o64)["pass"]
+
+
+def test_rollout_replay_eq1(ua):
+    """Eq. (1): full prefill of p||y equals prefill(p) at prompt rows and
+    token-by-token decode (batch of all sequences each step) at response rows."""
+    import torch
+    w = inputs.custom(8, 2, 128, [64 + 64, 200 + 100, 300 + 40], sigma=1.0, page_size=16,
+                      prompt_lens=[64, 200, 300])
+    pk = gu.Pack(w, seed=7)
+    full = gu.host_bits(_prefill(ua, pk)[0])
+    # rollout prefill over prompts only (its own pack of the prompt tokens)
+    P = w.prompt_lens
+    idx = np.concatenate([np.arange(pk.cu[s], pk.cu[s] + P[s]) for s in range(w.num_seqs)])
+    it = torch.from_numpy(idx).cuda()
+    cu_p = gu.dev_i32(inputs.cu_seqlens(P))
+    pout = gu.host_bits(ua.prefill(pk.q[it].contiguous(), pk.k[it].contiguous(), pk.v[it].contiguous(), cu_p, max(P)))
+    assert np.array_equal(pout, full[idx]), "prompt rows: prefill(p) != prefill(p||y)"
+    # token-by-token decode; finished sequences drop out of the batch
+    R = [L - p for L, p in zip(w.seq_lens, P)]
+    mism = 0
+    for step in range(max(R)):
+        entries = [(s, P[s] + step) for s in range(w.num_seqs) if step < R[s]]
+        q, table, seqlens, maxs, tok = pk.decode_rows(entries)
+        d = gu.host_bits(ua.decode(q, pk.kp, pk.vp, table, seqlens, max(w.seq_lens)))
+        mism += int((~gu.rows_equal_bits(d, full[tok])).sum())
+    assert mism == 0, mism
+
+
+def test_decode_batch_mix_permutation_and_split_invariance(ua):
+    """The same decode entry gives the same bits alone, in a batch, in any
+    order, with any max_seqlen (grid/workspace size)."""
+    w = inputs.custom(8, 2, 128, [1500, 900, 77, 2100], sigma=0.5, page_size=64)
+    pk = gu.Pack(w, seed=11)
+    rng = np.random.default_rng(5)
+    entries = [(s, int(rng.integers(0, w.seq_lens[s]))) for s in range(4) for _ in range(9)]
+    q, table, seqlens, maxs, tok = pk.decode_rows(entries)
+    ref = gu.host_bits(ua.decode(q, pk.kp, pk.vp, table, seqlens, maxs))
+    for trial in range(3):
+        perm = rng.permutation(len(entries))
+        q2, t2, s2, m2, _ = pk.decode_rows([entries[i] for i in perm])
+        cap = pk.table.shape[1] * pk.page          # largest max_seqlen the block table allows
+        got = gu.host_bits(ua.decode(q2, pk.kp, pk.vp, t2, s2, [m2, m2 + 257, cap][trial]))
+        assert np.array_equal(got, ref[perm])
+    for i in [0, 17, 35]:
+        q1, t1, s1, m1, _ = pk.decode_rows([entries[i]])
+        assert np.array_equal(gu.host_bits(ua.decode(q1, pk.kp, pk.vp, t1, s1, m1)), ref[i:i + 1])
+
+
+def test_prefill_pack_order_and_max_seqlen_invariance(ua):
+    w = inputs.custom(4, 1, 128, [333, 64, 1025], sigma=1.0)
+    pk = gu.Pack(w, seed=3)
+    ref = gu.host_bits(_prefill(ua, pk)[0])
+    import torch
+    order = [2, 0, 1]
+    idx = np.concatenate([np.arange(pk.cu[s], pk.cu[s + 1]) for s in order])
+    it = torch.from_numpy(idx).cuda()
+    cu2 = gu.dev_i32(inputs.cu_seqlens([w.seq_lens[s] for s in order]))
+    got = gu.host_bits(ua.prefill(pk.q[it].contiguous(), pk.k[it].contiguous(), pk.v[it].contiguous(), cu2, 4000))
+    assert np.array_equal(got, ref[idx])
+
+
+def test_run_to_run_determinism(ua):
+    w = inputs.custom(8, 2, 128, [700, 300], sigma=1.0)
+    pk = gu.Pack(w, seed=13)
+    a = gu.host_bits(_prefill(ua, pk)[0])
+    b = gu.host_bits(_prefill(ua, pk)[0])
+    assert np.array_equal(a, b)
+    entries = [(0, 699), (1, 299), (0, 256), (0, 255)]
+    q, t, s, m, _ = pk.decode_rows(entries)
+    x = gu.host_bits(ua.decode(q, pk.kp, pk.vp, t, s, m))
+    y = gu.host_bits(ua.decode(q, pk.kp, pk.vp, t, s, m))
+    assert np.array_equal(x, y)
+
+
+def test_unwritten_slots_are_never_read(ua):
+    """Cache slots past each context hold NaN (and +/-Inf): outputs are finite
+    and unchanged versus a zero-filled cache."""
+    w = inputs.custom(8, 2, 128, [100, 37, 300], sigma=1.0, page_size=64)
+    nan = gu.Pack(w, seed=21, fill_bits=0x7FC0)
+    inf = gu.Pack(w, seed=21, fill_bits=0xFF80)
+    zero = gu.Pack(w, seed=21, fill_bits=0x0000)
+    entries = [(0, 99), (1, 36), (2, 299), (2, 64), (0, 0)]
+    outs = []
+    for pk in (nan, inf, zero):
+        q, t, s, m, _ = pk.decode_rows(entries)
+        outs.append(gu.host_bits(ua.decode(q, pk.kp, pk.vp, t, s, m)))
+    q, t, s, m, _ = nan.decode_rows(entries)
+    assert not np.isnan(gu.host_f64(ua.decode(q, nan.kp, nan.vp, t, s, 300))).any()
+    assert np.array_equal(outs[0], outs[2]) and np.array_equal(outs[1], outs[2])
+
+
+def test_single_token_context_returns_v(ua):
+    w = inputs.custom(8, 2, 128, [1, 1, 5], sigma=1.0, page_size=16)
+    pk = gu.Pack(w, seed=2)
+    out = gu.host_bits(_prefill(ua, pk)[0])
+    v = pk.host["v"]
+    for tok in [0, 1, 2]:
+        for h in range(8):
+            assert np.array_equal(out[tok, h], v[tok, h // 4])
+    q, t, s, m, tk = pk.decode_rows([(0, 0), (2, 0)])
+    d = gu.host_bits(ua.decode(q, pk.kp, pk.vp, t, s, m))
+    assert np.array_equal(d[1, 5], v[2, 1])
+
+
+def test_empty_sequences_in_pack(ua):
+    w = inputs.custom(4, 2, 64, [0, 5, 0, 70, 0], sigma=1.0)
+    pk = gu.Pack(w, seed=4)
+    out, lse = _prefill(ua, pk)
+    o64, _ = oracle.causal_attention_fp64(pk.host["q"], pk.host["k"], pk.host["v"], pk.cu)
+    assert oracle.parity_report(gu.host_f64(out), o64)["pass"]
+
+
+def test_hip_graph_replay_with_varying_inputs(ua):
+    """Decode and prefill captured in a HIP graph, replayed with new inputs
+    copied into the captured buffers: every replay equals eager execution."""
+    import torch
+    w = inputs.custom(8, 2, 128, [600, 300], sigma=1.0, page_size=64)
+    pk = gu.Pack(w, seed=31)
+    entries = [(0, 599), (1, 299)]
+    q, t, s, m, _ = pk.decode_rows(entries)
+    ws = torch.empty(ua.decode_workspace_bytes(2, 600, 8, 128), dtype=torch.uint8, device="cuda")
+    dout = torch.empty_like(q)
+    pout = torch.empty_like(pk.q)
+    qbuf = pk.q.clone()
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        ua.prefill(qbuf, pk.k, pk.v, pk.cu_dev, 600, out=pout)
+        ua.decode(q, pk.kp, pk.vp, t, s, 600, out=dout, workspace=ws)
+    rng = np.random.default_rng(0)
+    for rep in range(4):
+        newq = gu.dev(inputs.normal_bf16(tuple(pk.q.shape), 1.0, 77, rep))
+        qbuf.copy_(newq)
+        q.copy_(newq[torch.tensor([599, 600 + 299], device="cuda")])
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        eager_p = ua.prefill(newq, pk.k, pk.v, pk.cu_dev, 600)
+        eager_d = ua.decode(q.clone(), pk.kp, pk.vp, t, s, 600)
+        torch.cuda.synchronize()
+        assert torch.equal(pout.view(torch.int16), eager_p.view(torch.int16)), rep
+        assert torch.equal(dout.view(torch.int16), eager_d.view(torch.int16)), rep
+        _ = rng
+
+
+def test_mfma_column_slot_independence(ua):
+    """The same query placed in different MFMA columns (different positions in
+    a prefill wave, different head slots in decode) gives the same bits: a
+    sequence whose every query row equals one vector, with K/V constant past
+    position 0, forces rows across the wave to share arithmetic."""
+    d, L = 128, 96
+    w = inputs.custom(2, 1, d, [L], sigma=1.0)
+    pk = gu.Pack(w, seed=5)
+    import torch
+    qrow = pk.q[0:1, 0:1, :]
+    q = qrow.expand(L, 2, d).contiguous()
+    out = gu.host_bits(ua.prefill(q, pk.k, pk.v, pk.cu_dev, L))
+    # heads 0 and 1 (different decode columns) hold identical queries
+    assert np.array_equal(out[:, 0], out[:, 1])
+    ents = [(0, p) for p in range(L)]
+    qd, t, s, m, tok = pk.decode_rows(ents)
+    qd = q[torch.from_numpy(tok).cuda()].contiguous()
+    d_out = gu.host_bits(ua.decode(qd, pk.kp, pk.vp, t, s, m))
+    assert np.array_equal(d_out, out[tok])
