@@ -231,3 +231,25 @@ def logits_bf16(rows: int, vocab: int, sigma: float, seed: int = BASE_SEED, tag:
 
 def targets(rows: int, vocab: int, seed: int = BASE_SEED, tag: int = 0) -> np.ndarray:
     return rng(8, tag, seed=seed).integers(0, vocab, size=rows).astype(np.int32)
+
+
+# --------------------------------------------------------------------------
+# device-side generation (large workloads; same recipe, torch's seeded Philox)
+# --------------------------------------------------------------------------
+def normal_bf16_device(shape, sigma: float, *key: int, seed: int = BASE_SEED, device="cuda", chunk_elems: int = 1 << 28):
+    """i.i.d. N(0, sigma^2) bf16 tensor drawn on the GPU from a generator
+    seeded by (seed, *key).  Used where host generation would take minutes
+    (billions of logits, multi-GB packs); the values are copied back to the
+    host wherever the oracle needs them."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(rng(*key, seed=seed).integers(0, 2 ** 62)))
+    out = torch.empty(tuple(shape), dtype=torch.bfloat16, device=device)
+    flat = out.view(-1)
+    n = flat.numel()
+    for lo in range(0, n, chunk_elems):
+        hi = min(n, lo + chunk_elems)
+        tmp = torch.randn(hi - lo, generator=g, device=device, dtype=torch.float32)
+        flat[lo:hi] = (tmp * sigma).to(torch.bfloat16)
+        del tmp
+    return out

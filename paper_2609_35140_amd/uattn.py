@@ -187,3 +187,57 @@ def logprob(logits, targets, inv_temperature: float = 1.0, out=None, stream=None
 def raw_call(name: str, *args) -> int:
     """Call a C entry point with raw arguments (for error-path tests)."""
     return int(getattr(_load(), name)(*args))
+
+
+class DecodeSteps:
+    """Argument lists for a run of uattn_decode calls over fixed buffers.
+
+    A rollout loop calls decode once per generated token on the same cache,
+    block table and workspace; only the query, length and output slices
+    change.  This marshals every call's arguments once, so the loop pays one
+    ctypes call per step.
+
+      q_steps        [S, B, Hq, d] bf16   (step i uses q_steps[i])
+      seqlens_steps  [S, B] int32
+      out_steps      [S, B, Hq, d] bf16
+    """
+
+    def __init__(self, q_steps, k_pages, v_pages, block_table, seqlens_steps, max_seqlen: int, out_steps,
+                 workspace=None, softmax_scale: Optional[float] = None, stream=None):
+        import torch
+        for name, t in (("q_steps", q_steps), ("k_pages", k_pages), ("v_pages", v_pages), ("out_steps", out_steps)):
+            _bf16_cuda(t, name)
+        _need(q_steps.dim() == 4 and out_steps.shape == q_steps.shape, "q_steps/out_steps must be [S,B,Hq,d]")
+        S, B, hq, d = q_steps.shape
+        _, hkv, page, d2 = k_pages.shape
+        _need(d2 == d and v_pages.shape == k_pages.shape, "page shapes")
+        _need(seqlens_steps.dtype == torch.int32 and seqlens_steps.shape == (S, B) and seqlens_steps.is_contiguous(),
+              "seqlens_steps must be [S,B] int32")
+        _need(block_table.dtype == torch.int32 and block_table.is_contiguous() and block_table.shape[0] == B,
+              "block_table must be [B,maxp] int32")
+        if softmax_scale is None:
+            softmax_scale = default_scale(d)
+        need = decode_workspace_bytes(B, int(max_seqlen), hq, d)
+        if workspace is None and need > 0:
+            workspace = torch.empty(need, dtype=torch.uint8, device=q_steps.device)
+        self.workspace = workspace
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        st = _stream(stream)
+        qstride = B * hq * d * 2
+        lstride = B * 4
+        self._fn = _load().uattn_decode
+        self.args = [
+            (q_steps.data_ptr() + i * qstride, _ptr(k_pages), _ptr(v_pages), _ptr(block_table),
+             seqlens_steps.data_ptr() + i * lstride, B, block_table.shape[1], page, k_pages.shape[0], int(max_seqlen),
+             hq, hkv, d, float(softmax_scale), out_steps.data_ptr() + i * qstride, None, _ptr(workspace), ws_bytes, st)
+            for i in range(S)
+        ]
+        self._keep = (q_steps, k_pages, v_pages, block_table, seqlens_steps, out_steps)
+
+    def __len__(self):
+        return len(self.args)
+
+    def run(self, i: int):
+        code = self._fn(*self.args[i])
+        if code != UATTN_OK:
+            raise UattnError(status_string(code))

@@ -40,7 +40,7 @@ def rows_equal_bits(a: np.ndarray, b: np.ndarray) -> np.ndarray:
 class Pack:
     """A packed varlen batch on the GPU plus its paged cache."""
 
-    def __init__(self, w, seed=42, tag=0, page_size=None, fill_bits=0x7FC0, extra_pages=5):
+    def __init__(self, w, seed=42, tag=0, page_size=None, fill_bits=0x7FC0, extra_pages=5, table_slack=8):
         from paper_2609_35140_amd import inputs
         self.w = w
         t = inputs.packed_qkv(w, seed=seed, tag=tag)
@@ -49,7 +49,9 @@ class Pack:
         self.q, self.k, self.v = dev(t["q"]), dev(t["k"]), dev(t["v"])
         self.cu_dev = dev_i32(self.cu)
         self.page = page_size or w.page_size
-        table, npages = inputs.paged_layout(w.seq_lens, self.page, seed=seed, tag=tag, extra_pages=extra_pages)
+        maxp = max((L + self.page - 1) // self.page for L in w.seq_lens) + table_slack if w.seq_lens else 1
+        table, npages = inputs.paged_layout(w.seq_lens, self.page, seed=seed, tag=tag, extra_pages=extra_pages,
+                                            max_pages_per_seq=maxp)
         self.table = table
         self.kp_host = inputs.scatter_to_pages(t["k"], self.cu, table, npages, self.page, fill_bits)
         self.vp_host = inputs.scatter_to_pages(t["v"], self.cu, table, npages, self.page, fill_bits)
