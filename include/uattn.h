@@ -117,13 +117,21 @@ size_t uattn_decode_workspace_bytes(int32_t batch, int32_t max_seqlen, int32_t n
  *   lse          [batch, num_q_heads] fp32, or NULL
  *   workspace    device scratch of at least
  *                uattn_decode_workspace_bytes(batch, max_seqlen, Hq, d) bytes
- *                (may be NULL when that is 0); contents need no initialization
- *                and are overwritten.  Calls that share a workspace must be
- *                ordered on one stream.
+ *                (may be NULL when that is 0), 16-byte aligned.  Its first
+ *                C = round_up(4 * batch * num_q_heads, 256) bytes hold one
+ *                arrival counter per (entry, kv head); the fp32 chunk
+ *                partials go at its end.  The C counter bytes must be zero
+ *                when a call starts.  Every call leaves its own counter bytes
+ *                zero again (also under HIP graph replay), so: zero-fill a
+ *                new workspace once, and zero it again only before a call
+ *                whose C is larger than the previous call's on the same
+ *                workspace (or after an aborted call).  Calls that share a
+ *                workspace must be ordered on one stream.
  *
  * Keys are split into fixed 256-position chunks; each chunk's partial
- * softmax state is folded in ascending chunk order, so results do not depend
- * on the batch, its order or the split.  (num_q_heads / num_kv_heads) <= 32.
+ * softmax state is folded in ascending chunk order (by whichever workgroup
+ * finishes an entry's last chunk), so results do not depend on the batch,
+ * its order or the split.  (num_q_heads / num_kv_heads) <= 32.
  */
 uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_pages,
                           const int32_t* block_table, const int32_t* seqlens, int32_t batch,

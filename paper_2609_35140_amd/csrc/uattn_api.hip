@@ -94,7 +94,8 @@ size_t uattn_decode_workspace_bytes(int32_t batch, int32_t max_seqlen, int32_t n
   if (batch <= 0 || max_seqlen <= 0 || num_q_heads <= 0 || head_dim <= 0) return 0;
   const int64_t nchunk = (static_cast<int64_t>(max_seqlen) + kChunkKeys - 1) / kChunkKeys;
   if (nchunk <= 1) return 0;
-  return uattn::decode_ws_acc_bytes(batch, nchunk, num_q_heads, head_dim) +
+  return uattn::decode_ws_cnt_bytes(batch, num_q_heads) +
+         uattn::decode_ws_acc_bytes(batch, nchunk, num_q_heads, head_dim) +
          uattn::decode_ws_ml_bytes(batch, nchunk, num_q_heads);
 }
 
@@ -140,10 +141,22 @@ uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_page
   a.seqlens = seqlens;
   a.out = out;
   a.lse = lse;
-  a.ws_acc = static_cast<float*>(workspace);
-  a.ws_ml = need > 0 ? reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                                uattn::decode_ws_acc_bytes(batch, nchunk, num_q_heads, head_dim))
-                     : nullptr;
+  // counters at the start, partials at the end of the caller's buffer: a
+  // workspace sized for one call can be reused by any call it is large enough for
+  // without a partial region ever covering a counter that a later call relies on
+  // being zero (see the zero-fill rule in uattn.h)
+  if (need > 0) {
+    const size_t acc_b = uattn::decode_ws_acc_bytes(batch, nchunk, num_q_heads, head_dim);
+    const size_t ml_b = uattn::decode_ws_ml_bytes(batch, nchunk, num_q_heads);
+    char* end = static_cast<char*>(workspace) + (workspace_bytes & ~static_cast<size_t>(15));
+    a.ws_cnt = static_cast<int32_t*>(workspace);
+    a.ws_ml = reinterpret_cast<float*>(end - ml_b);
+    a.ws_acc = reinterpret_cast<float*>(end - ml_b - acc_b);
+  } else {
+    a.ws_cnt = nullptr;
+    a.ws_ml = nullptr;
+    a.ws_acc = nullptr;
+  }
   a.batch = batch;
   a.max_pages_per_seq = max_pages_per_seq;
   a.page_size = page_size;

@@ -1,18 +1,21 @@
 // Token-wise decode entry point: one query per sequence against a paged KV cache.
 //
-// Split kernel: workgroup = (256-key positional chunk, kv head, batch entry).
+// One kernel: workgroup = (256-key positional chunk, kv head, batch entry).
 // The G query heads of the kv head sit in the MFMA columns (padded to 32), so
 // each K/V tile is read from HBM once for the whole group.  The four waves
 // compute the same scores and softmax state (the shared per-tile sequence of
 // uattn_numerics.h) and each accumulates one 32-wide d block of the output.
 // A chunk's result is either final (the context fits in one chunk) or an
-// fp32 partial (m, l, acc) written to the workspace.
+// fp32 partial (m, l, acc) written to the workspace.  The page-table entries of
+// the chunk are fetched up front and two tiles are kept in flight.
 //
-// Merge kernel: folds an entry's chunk partials left to right in chunk order
-// and normalizes -- the same fold, in the same order, that the full-sequence
-// kernel applies at its chunk boundaries.  Chunk boundaries depend only on
-// key positions, so nothing here depends on the batch, its order, the grid or
-// max_seqlen.
+// Merge: the workgroup that completes an entry's last outstanding chunk
+// (an arrival counter per (entry, kv head), reset to zero after use) folds
+// the entry's chunk partials left to right in chunk order and normalizes --
+// the same fold, in the same order, that the full-sequence kernel applies at
+// its chunk boundaries.  Chunk boundaries depend only on key positions, so
+// nothing here depends on the batch, its order, the grid, max_seqlen or which
+// workgroup merges.
 #include "uattn_internal.h"
 #include "uattn_numerics.h"
 #include "uattn_tile_io.h"
@@ -28,16 +31,58 @@ struct DecodeParams {
   const int32_t* seqlens;
   __bf16* out;
   float* lse;
-  float* ws_acc;
-  float* ws_ml;
+  float* ws_acc;     // [batch][Hq][nchunk_max][D]
+  float* ws_ml;      // [batch][Hq][nchunk_max][2]
+  int32_t* ws_cnt;   // [batch][Hkv] arrival counters, zero between calls
   int hq, hkv, group, maxp, page_size, num_pages, max_seqlen, nchunk_max;
   float c;
 };
 
+// Partials cross workgroups (and XCDs, whose L2 caches are not coherent with
+// each other for ordinary stores).  They are written and read with
+// agent-scope relaxed atomic accesses, which go through to the device-
+// coherent level, instead of full-cache release/acquire fences (an L2
+// writeback and invalidate per workgroup).  Ordering: every writer waits
+// for its stores to complete before the workgroup barrier, one thread then
+// bumps the arrival counter; the merger reads the partials only after its
+// counter increment has returned the final count.
+__device__ __forceinline__ void st_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coherent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Fold the chunk partials of entry b, kv head kvh (all its q heads) in chunk
+// order and write the normalized outputs.  Called by the workgroup that
+// finished the entry's last outstanding chunk.
 template <int D>
-__global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeParams p) {
-  constexpr int NDB = D / 32;
+__device__ __forceinline__ void merge_entry(const DecodeParams& p, int b, int kvh, int nch, int tid) {
+  const int nvals = p.group * D;
+  for (int v = tid; v < nvals; v += 256) {
+    const int g = v / D, d = v % D;
+    const int head = kvh * p.group + g;
+    const int64_t base = (static_cast<int64_t>(b) * p.hq + head) * p.nchunk_max;
+    const float* ml = p.ws_ml + base * 2;
+    const float* ac = p.ws_acc + base * D + d;
+    float M = ld_coherent(ml), L = ld_coherent(ml + 1), A = ld_coherent(ac);
+#pragma unroll 4
+    for (int k = 1; k < nch; ++k) {
+      const FoldScale f = fold_scale(M, ld_coherent(ml + 2 * k), p.c);
+      L = fold_val(f, L, ld_coherent(ml + 2 * k + 1));
+      A = fold_val(f, A, ld_coherent(ac + static_cast<int64_t>(k) * D));
+      M = f.m_new;
+    }
+    p.out[(static_cast<int64_t>(b) * p.hq + head) * D + d] = finalize_val(A, L);
+    if (p.lse != nullptr && d == 0) p.lse[static_cast<int64_t>(b) * p.hq + head] = finalize_lse(M, L, p.c);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
   __shared__ __attribute__((aligned(16))) __bf16 lds[2 * Lds<D>::kStageElems];
+  __shared__ int s_last;
+  constexpr int NDB = D / 32;
 
   const int chunk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int n = min(p.seqlens[b], p.max_seqlen);  // clamp (trusted) lengths to the sized grid
@@ -45,12 +90,27 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeParams p) {
   if (n < 1 || chunk >= nch) return;
   const int t0 = chunk * kTilesPerChunk;
   const int last_tile = (n - 1) / kTileKeys;
-  const int t1 = min(t0 + kTilesPerChunk - 1, last_tile);
+  const int ntiles = min(kTilesPerChunk, last_tile - t0 + 1);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const int qpos = n - 1;
   const int head = kvh * p.group + col;
+
+  // Where this thread's rows of each tile of the chunk live.  A thread's
+  // kKPU consecutive rows always share one page (pages are >= 16 keys).
+  const int r0 = TileIO<D>::first_row(tid);
+  const int32_t* bt_row = p.bt + static_cast<int64_t>(b) * p.maxp;
+  int64_t off0[kTilesPerChunk];
+  int nvalid[kTilesPerChunk];
+#pragma unroll
+  for (int j = 0; j < kTilesPerChunk; ++j) {
+    const int pos = (t0 + j) * kTileKeys + r0;
+    const int64_t page = (j < ntiles && pos < n) ? bt_row[pos / p.page_size] : -1;
+    const bool ok = page >= 0 && page < p.num_pages;
+    off0[j] = ok ? ((page * p.hkv + kvh) * p.page_size + (pos % p.page_size)) * D : 0;
+    nvalid[j] = ok ? n - pos : 0;
+  }
 
   bf16x8 qf[D / 16];
   if (col < p.group) {
@@ -64,17 +124,10 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeParams p) {
       for (int e = 0; e < 8; ++e) qf[st][e] = static_cast<__bf16>(0.0f);
   }
 
-  TileIO<D> io;
-  const int r0 = TileIO<D>::first_row(tid);
-  const int32_t* bt_row = p.bt + static_cast<int64_t>(b) * p.maxp;
-  auto row_offsets = [&](int t, int64_t (&offs)[TileIO<D>::kKPU]) {
-#pragma unroll
-    for (int i = 0; i < TileIO<D>::kKPU; ++i) {
-      const int pos = t * kTileKeys + r0 + i;
-      const int64_t page = pos < n ? bt_row[pos / p.page_size] : -1;
-      offs[i] = (page >= 0 && page < p.num_pages) ? ((page * p.hkv + kvh) * p.page_size + (pos % p.page_size)) * D : -1;
-    }
-  };
+  // two tiles in flight in registers, two LDS stages
+  TileIO<D> io[2];
+  io[0].load(p.kp, p.vp, off0[0], D, nvalid[0], tid);
+  if (ntiles > 1) io[1].load(p.kp, p.vp, off0[1], D, nvalid[1], tid);
 
   f32x16 acc[1];
 #pragma unroll
@@ -83,31 +136,26 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeParams p) {
   const float c = p.c;
   const bool pv_on = wave < NDB;
 
-  {
-    int64_t offs[TileIO<D>::kKPU];
-    row_offsets(t0, offs);
-    io.load(p.kp, p.vp, offs, tid);
-  }
-  for (int t = t0; t <= t1; ++t) {
-    __bf16* stage = lds + ((t - t0) & 1) * Lds<D>::kStageElems;
-    io.store(stage, tid);
-    __syncthreads();
-    if (t < t1) {
-      int64_t offs[TileIO<D>::kKPU];
-      row_offsets(t + 1, offs);
-      io.load(p.kp, p.vp, offs, tid);
+#pragma unroll
+  for (int j = 0; j < kTilesPerChunk; ++j) {
+    if (j < ntiles) {
+      __bf16* stage = lds + (j & 1) * Lds<D>::kStageElems;
+      io[j & 1].store(stage, tid);
+      __syncthreads();
+      if (j + 2 < ntiles) io[j & 1].load(p.kp, p.vp, off0[j + 2], D, nvalid[j + 2], tid);
+      const int t = t0 + j;
+      f32x16 s[2];
+      qk_scores<D>(stage, qf, s, lane);
+      if (t == last_tile) mask_scores(s, t * kTileKeys, qpos, lane);
+      const float alpha = softmax_tile(s, m, l, c);
+      bf16x8 pb[4];
+      pack_p(s, pb);
+      if (pv_on) pv_tile<D, 1>(stage + Lds<D>::kKElems, pb, acc, alpha, wave, lane);
     }
-    f32x16 s[2];
-    qk_scores<D>(stage, qf, s, lane);
-    if (t == last_tile) mask_scores(s, t * kTileKeys, qpos, lane);
-    const float alpha = softmax_tile(s, m, l, c);
-    bf16x8 pb[4];
-    pack_p(s, pb);
-    if (pv_on) pv_tile<D, 1>(stage + Lds<D>::kKElems, pb, acc, alpha, wave, lane);
   }
 
-  if (!pv_on || col >= p.group) return;
   if (nch == 1) {
+    if (!pv_on || col >= p.group) return;
     __bf16* orow = p.out + (static_cast<int64_t>(b) * p.hq + head) * D + 32 * wave;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -117,57 +165,51 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeParams p) {
       *reinterpret_cast<bf16x4*>(orow + 8 * i + 4 * h) = w;
     }
     if (p.lse != nullptr && wave == 0 && h == 0) p.lse[static_cast<int64_t>(b) * p.hq + head] = finalize_lse(m, l, c);
-  } else {
+    return;
+  }
+
+  // chunk partial -> workspace
+  if (pv_on && col < p.group) {
     const int64_t slot = (static_cast<int64_t>(b) * p.hq + head) * p.nchunk_max + chunk;
     float* arow = p.ws_acc + slot * D + 32 * wave;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<f32x4*>(arow + 8 * i + 4 * h) =
-          f32x4{acc[0][4 * i], acc[0][4 * i + 1], acc[0][4 * i + 2], acc[0][4 * i + 3]};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) st_coherent(arow + 8 * i + 4 * h + j, acc[0][4 * i + j]);
     if (wave == 0 && h == 0) {
-      p.ws_ml[slot * 2] = m;
-      p.ws_ml[slot * 2 + 1] = l;
+      st_coherent(p.ws_ml + slot * 2, m);
+      st_coherent(p.ws_ml + slot * 2 + 1, l);
     }
   }
-}
-
-// One workgroup of 64 threads per (q head, entry); thread t owns d = t + 64*j.
-template <int D>
-__global__ __launch_bounds__(64) void decode_merge_kernel(DecodeParams p) {
-  constexpr int PER = D / 64;
-  const int head = blockIdx.x, b = blockIdx.y;
-  const int n = min(p.seqlens[b], p.max_seqlen);
-  const int nch = (n + kChunkKeys - 1) / kChunkKeys;
-  if (n < 1 || nch <= 1) return;
-  const int tid = threadIdx.x;
-  const int64_t base = (static_cast<int64_t>(b) * p.hq + head) * p.nchunk_max;
-  const float* ml = p.ws_ml + base * 2;
-  const float* ac = p.ws_acc + base * D;
-  const float c = p.c;
-  float M = ml[0], L = ml[1];
-  float A[PER];
-#pragma unroll
-  for (int j = 0; j < PER; ++j) A[j] = ac[tid + 64 * j];
-  for (int k = 1; k < nch; ++k) {
-    const FoldScale f = fold_scale(M, ml[2 * k], c);
-    L = fold_val(f, L, ml[2 * k + 1]);
-#pragma unroll
-    for (int j = 0; j < PER; ++j) A[j] = fold_val(f, A[j], ac[static_cast<int64_t>(k) * D + tid + 64 * j]);
-    M = f.m_new;
+  // The workgroup that completes the entry's last outstanding chunk folds
+  // them all.  Which workgroup that is does not affect the arithmetic: the
+  // fold order is the chunk order.
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
+  __syncthreads();
+  if (tid == 0) {
+    const int prev = __hip_atomic_fetch_add(p.ws_cnt + static_cast<int64_t>(b) * p.hkv + kvh, 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == nch - 1);
   }
-  __bf16* orow = p.out + (static_cast<int64_t>(b) * p.hq + head) * D;
-#pragma unroll
-  for (int j = 0; j < PER; ++j) orow[tid + 64 * j] = finalize_val(A[j], L);
-  if (p.lse != nullptr && tid == 0) p.lse[static_cast<int64_t>(b) * p.hq + head] = finalize_lse(M, L, c);
+  __syncthreads();
+  if (!s_last) return;
+  merge_entry<D>(p, b, kvh, nch, tid);
+  if (tid == 0)
+    __hip_atomic_store(p.ws_cnt + static_cast<int64_t>(b) * p.hkv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace
 
 size_t decode_ws_acc_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads, int64_t head_dim) {
-  return static_cast<size_t>(batch * num_q_heads * nchunk_max * head_dim) * sizeof(float);
+  return (static_cast<size_t>(batch * num_q_heads * nchunk_max * head_dim) * sizeof(float) + 255) / 256 * 256;
 }
 size_t decode_ws_ml_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads) {
-  return static_cast<size_t>(batch * num_q_heads * nchunk_max * 2) * sizeof(float);
+  return (static_cast<size_t>(batch * num_q_heads * nchunk_max * 2) * sizeof(float) + 255) / 256 * 256;
+}
+// Counters are sized by the q-head count (an upper bound of the kv-head count)
+// so that the size depends only on the arguments of uattn_decode_workspace_bytes.
+size_t decode_ws_cnt_bytes(int64_t batch, int64_t num_q_heads) {
+  return (static_cast<size_t>(batch * num_q_heads) * sizeof(int32_t) + 255) / 256 * 256;
 }
 
 hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
@@ -181,6 +223,7 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
   p.lse = a.lse;
   p.ws_acc = a.ws_acc;
   p.ws_ml = a.ws_ml;
+  p.ws_cnt = a.ws_cnt;
   p.hq = a.num_q_heads;
   p.hkv = a.num_kv_heads;
   p.group = a.num_q_heads / a.num_kv_heads;
@@ -192,16 +235,9 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
   p.c = a.c;
   const dim3 grid(a.nchunk_max, a.num_kv_heads, a.batch);
   if (a.head_dim == 128)
-    hipLaunchKernelGGL(decode_split_kernel<128>, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(decode_kernel<128>, grid, dim3(256), 0, stream, p);
   else
-    hipLaunchKernelGGL(decode_split_kernel<64>, grid, dim3(256), 0, stream, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.nchunk_max <= 1) return e;
-  const dim3 mgrid(a.num_q_heads, a.batch);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(64), 0, stream, p);
-  else
-    hipLaunchKernelGGL(decode_merge_kernel<64>, mgrid, dim3(64), 0, stream, p);
+    hipLaunchKernelGGL(decode_kernel<64>, grid, dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -33,6 +33,7 @@ struct DecodeLaunch {
   float* lse;
   float* ws_acc;  // [batch][Hq][nchunk_max][head_dim]
   float* ws_ml;   // [batch][Hq][nchunk_max][2]
+  int32_t* ws_cnt; // [batch][Hkv] arrival counters
   int32_t batch;
   int32_t max_pages_per_seq;
   int32_t page_size;
@@ -60,8 +61,10 @@ hipError_t launch_prefill(const PrefillLaunch& a, hipStream_t stream);
 hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream);
 hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t stream);
 
-// Decode workspace split (bytes of the acc part; the m/l part follows it).
+// Decode workspace: arrival counters at the start (kept zero between calls),
+// the fp32 partials (acc, then m/l) at the end of the caller's buffer.
 size_t decode_ws_acc_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads, int64_t head_dim);
 size_t decode_ws_ml_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads);
+size_t decode_ws_cnt_bytes(int64_t batch, int64_t num_q_heads);
 
 }  // namespace uattn

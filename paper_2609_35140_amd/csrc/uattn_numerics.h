@@ -56,13 +56,15 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// LDS row strides (elements).  K tile: [64 keys][D + 8]; V^T tile: [D][64 + 8].
-// The 16-byte pad keeps 16-lane groups of 128-bit reads on distinct banks.
+// LDS row strides (elements).  K tile: [64 keys][D + 8]; V tile: [64 keys][kVStride].
+// Both tiles are stored key-major as they come from memory.  The K pad keeps
+// 16-lane groups of 128-bit reads on distinct banks; the V stride keeps the
+// 32-lane groups of transposing 64-bit reads (see pv_tile) on distinct banks.
 template <int D> struct Lds {
   static constexpr int kKStride = D + 8;
-  static constexpr int kVStride = kTileKeys + 8;
+  static constexpr int kVStride = D == 128 ? 160 : 96;
   static constexpr int kKElems = kTileKeys * kKStride;
-  static constexpr int kVElems = D * kVStride;
+  static constexpr int kVElems = kTileKeys * kVStride;
   static constexpr int kStageElems = kKElems + kVElems;
 };
 
@@ -80,7 +82,7 @@ __device__ __forceinline__ __bf16 to_bf16(float x) { return static_cast<__bf16>(
 // 8*(r/4) + 4*h + r%4 of the 32-row block.  Rows are keys; which key each
 // A-operand row carries is chosen so that, after the in-lane regrouping of
 // p into the PV operand, every 8 consecutive K slots of the PV product are 8
-// consecutive keys (one 16-byte read of the transposed V tile).
+// consecutive keys (two transposing reads of the V tile, 4 keys each).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ constexpr int score_key(int blk, int r, int h) {
   return 32 * blk + 16 * ((r >> 2) >> 1) + 8 * h + 4 * ((r >> 2) & 1) + (r & 3);
@@ -172,19 +174,35 @@ __device__ __forceinline__ void pack_p(const f32x16 (&p)[2], bf16x8 (&pb)[4]) {
 }
 
 // acc[db] (O^T block db0+db: rows d, cols queries) <- alpha*acc + V^T_db P^T.
-//   vt_lds : V^T tile in LDS, [D][Lds<D>::kVStride]
+//   vs_lds : V tile in LDS, key-major [64][Lds<D>::kVStride]
+// The A operand (row d, K slots = keys 16*st + 8*h + e) is gathered with the
+// transposing 64-bit LDS read: within each 16-lane group, lane 4a+b receives
+// element b of the 4-element rows addressed by lanes a, a+4, a+8, a+12.  So
+// source lane s addresses key (base + s/4) at column (group's d base + 4*(s%4)),
+// and lane i of the group receives column d base + i for four consecutive keys.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+}
 template <int D, int NDB>
-__device__ __forceinline__ void pv_tile(const __bf16* vt_lds, const bf16x8 (&pb)[4], f32x16 (&acc)[NDB], float alpha,
+__device__ __forceinline__ void pv_tile(const __bf16* vs_lds, const bf16x8 (&pb)[4], f32x16 (&acc)[NDB], float alpha,
                                         int db0, int lane) {
-  const int h = lane >> 5, row = lane & 31;
+  const int g = lane >> 4, s = lane & 15;
+  const int h = g >> 1;
+  const int key0 = 8 * h + (s >> 2);
+  const int col0 = 16 * (g & 1) + 4 * (s & 3);
 #pragma unroll
   for (int db = 0; db < NDB; ++db) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[db][r] = alpha * acc[db][r];
-    const __bf16* vrow = vt_lds + (32 * (db0 + db) + row) * Lds<D>::kVStride + 8 * h;
+    const __bf16* vb = vs_lds + key0 * Lds<D>::kVStride + 32 * (db0 + db) + col0;
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(vrow + 16 * st);
+      const s16x4 lo = lds_read_tr16(vb + (16 * st) * Lds<D>::kVStride);
+      const s16x4 hi = lds_read_tr16(vb + (16 * st + 4) * Lds<D>::kVStride);
+      const s16x4 w[2] = {lo, hi};
+      bf16x8 a;
+      __builtin_memcpy(&a, w, sizeof(a));
       acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[st], acc[db], 0, 0, 0);
     }
   }

@@ -70,12 +70,10 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillParams p) {
 
   TileIO<D> io;
   const int r0 = TileIO<D>::first_row(tid);
-  auto row_offsets = [&](int t, int64_t (&offs)[TileIO<D>::kKPU]) {
-#pragma unroll
-    for (int i = 0; i < TileIO<D>::kKPU; ++i) {
-      const int pos = t * kTileKeys + r0 + i;
-      offs[i] = pos < L ? (static_cast<int64_t>(lo + pos) * p.hkv + kvh) * D : -1;
-    }
+  const int64_t row_stride = static_cast<int64_t>(p.hkv) * D;
+  auto load_tile = [&](int t) {
+    const int pos = t * kTileKeys + r0;
+    io.load(p.k, p.v, (static_cast<int64_t>(lo + pos) * p.hkv + kvh) * D, row_stride, L - pos, tid);
   };
 
   f32x16 acc[NDB], A[NDB];
@@ -89,20 +87,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillParams p) {
   float m = neg_inf(), l = 0.f, M = neg_inf(), Ls = 0.f;
   const float c = p.c;
 
-  {
-    int64_t offs[TileIO<D>::kKPU];
-    row_offsets(0, offs);
-    io.load(p.k, p.v, offs, tid);
-  }
+  load_tile(0);
   for (int t = 0; t <= wg_last_tile; ++t) {
     __bf16* stage = lds + (t & 1) * Lds<D>::kStageElems;
     io.store(stage, tid);
     __syncthreads();
-    if (t < wg_last_tile) {
-      int64_t offs[TileIO<D>::kKPU];
-      row_offsets(t + 1, offs);
-      io.load(p.k, p.v, offs, tid);
-    }
+    if (t < wg_last_tile) load_tile(t + 1);
     if (wave_on && t <= my_last_tile) {
       f32x16 s[2];
       qk_scores<D>(stage, qf, s, lane);

@@ -132,13 +132,39 @@ def decode_workspace_bytes(batch: int, max_seqlen: int, num_q_heads: int, head_d
     return int(_load().uattn_decode_workspace_bytes(batch, max_seqlen, num_q_heads, head_dim))
 
 
+def new_workspace(nbytes: int, device="cuda"):
+    """A zero-filled decode workspace (the counters it holds must start at zero)."""
+    import torch
+    return torch.zeros(int(nbytes), dtype=torch.uint8, device=device)
+
+
+def counter_bytes(batch: int, num_q_heads: int) -> int:
+    """Size of the counter region at the start of a decode workspace."""
+    return (4 * batch * num_q_heads + 255) // 256 * 256
+
+
+# counter-region size of the last call on each caller-provided workspace
+_ws_counter_extent = {}
+
+
+def _prepare_workspace(workspace, batch: int, num_q_heads: int):
+    """Zero the counter region of a caller-provided workspace when the uattn.h
+    rule requires it: first use here, or a larger region than the last call."""
+    key = workspace.data_ptr()
+    c = min(counter_bytes(batch, num_q_heads), workspace.numel() * workspace.element_size())
+    if _ws_counter_extent.get(key, -1) < c:
+        workspace.view(-1).view(dtype=workspace.dtype)[: c // workspace.element_size()].zero_()
+    _ws_counter_extent[key] = c
+
+
 def decode(q, k_pages, v_pages, block_table, seqlens, max_seqlen: int, softmax_scale: Optional[float] = None,
            out=None, return_lse: bool = False, lse=None, workspace=None, stream=None):
     """Token-wise paged decode (uattn_decode).
 
     q [B,Hq,d]; k_pages/v_pages [P,Hkv,page,d] bf16 CUDA; block_table [B,maxp]
     int32; seqlens [B] int32 (context length including the current token).
-    ``workspace`` is a uint8 CUDA tensor; allocated here when not given.
+    ``workspace`` is a zero-filled uint8 CUDA tensor (``new_workspace``); a
+    fresh one is allocated when not given.
     """
     import torch
     for name, t in (("q", q), ("k_pages", k_pages), ("v_pages", v_pages)):
@@ -161,7 +187,10 @@ def decode(q, k_pages, v_pages, block_table, seqlens, max_seqlen: int, softmax_s
         lse = torch.empty((B, hq), dtype=torch.float32, device=q.device)
     need = decode_workspace_bytes(B, int(max_seqlen), hq, d) if B > 0 else 0
     if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        workspace = new_workspace(need, q.device)
+        _ws_counter_extent[workspace.data_ptr()] = counter_bytes(B, hq)
+    elif workspace is not None and need > 0:
+        _prepare_workspace(workspace, B, hq)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_load().uattn_decode(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table), _ptr(seqlens), B,
                                 block_table.shape[1], page, k_pages.shape[0], int(max_seqlen), hq, hkv, d, float(softmax_scale),
@@ -219,7 +248,9 @@ class DecodeSteps:
             softmax_scale = default_scale(d)
         need = decode_workspace_bytes(B, int(max_seqlen), hq, d)
         if workspace is None and need > 0:
-            workspace = torch.empty(need, dtype=torch.uint8, device=q_steps.device)
+            workspace = new_workspace(need, q_steps.device)
+        elif workspace is not None and need > 0:
+            _prepare_workspace(workspace, B, hq)
         self.workspace = workspace
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         st = _stream(stream)

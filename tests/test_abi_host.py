@@ -50,11 +50,17 @@ def test_abi_version_and_status_strings(lib):
     assert "UNKNOWN" in uattn.status_string(99)
 
 
+def _r256(x):
+    return (x + 255) // 256 * 256
+
+
 def test_workspace_bytes(lib):
     from paper_2609_35140_amd import uattn
     assert uattn.decode_workspace_bytes(8, 256, 32, 128) == 0        # one chunk: no partials
-    assert uattn.decode_workspace_bytes(8, 257, 32, 128) == 8 * 32 * 2 * (128 + 2) * 4
-    assert uattn.decode_workspace_bytes(8, 4096, 32, 128) == 8 * 32 * 16 * 130 * 4
+    # counters [B*Hq int32] + acc [B*Hq*nchunk*d fp32] + (m, l) [B*Hq*nchunk*2 fp32], each 256-aligned
+    assert uattn.decode_workspace_bytes(8, 257, 32, 128) == _r256(8 * 32 * 4) + 8 * 32 * 2 * 128 * 4 + _r256(8 * 32 * 2 * 2 * 4)
+    assert uattn.decode_workspace_bytes(8, 4096, 32, 128) == _r256(8 * 32 * 4) + 8 * 32 * 16 * 128 * 4 + _r256(8 * 32 * 16 * 2 * 4)
+    assert uattn.decode_workspace_bytes(3, 300, 5, 64) == _r256(3 * 5 * 4) + _r256(3 * 5 * 2 * 64 * 4) + _r256(3 * 5 * 2 * 2 * 4)
     assert uattn.decode_workspace_bytes(0, 4096, 32, 128) == 0
     assert uattn.decode_workspace_bytes(1, -5, 32, 128) == 0
 

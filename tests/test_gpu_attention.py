@@ -196,7 +196,7 @@ def test_hip_graph_replay_with_varying_inputs(ua):
     pk = gu.Pack(w, seed=31)
     entries = [(0, 599), (1, 299)]
     q, t, s, m, _ = pk.decode_rows(entries)
-    ws = torch.empty(ua.decode_workspace_bytes(2, 600, 8, 128), dtype=torch.uint8, device="cuda")
+    ws = ua.new_workspace(ua.decode_workspace_bytes(2, 600, 8, 128))
     dout = torch.empty_like(q)
     pout = torch.empty_like(pk.q)
     qbuf = pk.q.clone()
@@ -241,3 +241,25 @@ def test_mfma_column_slot_independence(ua):
     qd = q[torch.from_numpy(tok).cuda()].contiguous()
     d_out = gu.host_bits(ua.decode(qd, pk.kp, pk.vp, t, s, m))
     assert np.array_equal(d_out, out[tok])
+
+
+def test_workspace_reuse_across_batch_sizes(ua):
+    """One zero-filled workspace serves a run of calls of different batch sizes
+    and lengths; results equal those with fresh workspaces, and the counter
+    words are zero after every call."""
+    import torch
+    w = inputs.custom(8, 2, 128, [2100, 900, 1500, 300, 1800], sigma=0.5, page_size=64)
+    pk = gu.Pack(w, seed=17)
+    rng = np.random.default_rng(9)
+    big = ua.decode_workspace_bytes(40, 2100, 8, 128)
+    ws = ua.new_workspace(big)
+    for trial, nb in enumerate([40, 7, 40, 3, 25, 1]):
+        ents = [(int(s), int(rng.integers(0, w.seq_lens[s]))) for s in rng.integers(0, 5, size=nb)]
+        q, t, s, m, _ = pk.decode_rows(ents)
+        maxs = [2100, m, 2100, m, 1024 if m <= 1024 else m, m][trial]
+        got = ua.decode(q, pk.kp, pk.vp, t, s, maxs, workspace=ws)
+        ref = ua.decode(q, pk.kp, pk.vp, t, s, maxs)
+        assert torch.equal(got.view(torch.int16), ref.view(torch.int16)), trial
+        torch.cuda.synchronize()
+        cnt = ws[: ua.counter_bytes(nb, 8)].view(torch.int32)
+        assert int(cnt.abs().sum().item()) == 0, trial
