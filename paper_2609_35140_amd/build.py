@@ -50,8 +50,9 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(resource_usage: bool = False, out: str = LIB, verbose: bool = False) -> str:
-    cmd = [hipcc(), *COMMON_FLAGS, "-shared", f"-I{INCLUDE}", f"-I{CSRC}", *sources(), "-o", out + ".tmp"]
+def build(resource_usage: bool = False, out: str = LIB, verbose: bool = False, defines=()) -> str:
+    cmd = [hipcc(), *COMMON_FLAGS, *[f"-D{d}" for d in defines], "-shared", f"-I{INCLUDE}", f"-I{CSRC}", *sources(),
+           "-o", out + ".tmp"]
     if resource_usage:
         cmd.insert(1, "-Rpass-analysis=kernel-resource-usage")
     if verbose:

@@ -63,7 +63,6 @@ uattn_status uattn_prefill(const void* q, const void* k, const void* v, const in
   if (num_seqs == 0 || total_tokens == 0 || max_seqlen == 0) return UATTN_OK;
   if (!q || !k || !v || !cu_seqlens || !out) return UATTN_EINVAL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return UATTN_EINVAL;
-  if ((static_cast<int64_t>(max_seqlen) + 127) / 128 > 65535) return UATTN_EUNSUPPORTED;
   if (validate_env()) {
     std::vector<int32_t> cu;
     if (!copy_back(cu, cu_seqlens, static_cast<size_t>(num_seqs) + 1)) return UATTN_EINVAL;
@@ -110,7 +109,7 @@ uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_page
   if (num_q_heads % num_kv_heads != 0 || !scale_ok(softmax_scale)) return UATTN_EINVAL;
   if (head_dim != 64 && head_dim != 128) return UATTN_EUNSUPPORTED;
   if (page_size < 16 || (page_size & (page_size - 1)) != 0) return UATTN_EUNSUPPORTED;
-  if (num_q_heads / num_kv_heads > uattn::kQCols) return UATTN_EUNSUPPORTED;
+  if (num_q_heads / num_kv_heads > uattn::kMaxGroup) return UATTN_EUNSUPPORTED;
   if (batch > 65535 || num_kv_heads > 65535) return UATTN_EUNSUPPORTED;
   if (batch == 0) return UATTN_OK;
   if (max_seqlen == 0 || num_pages == 0) return UATTN_EINVAL;  // every entry holds at least its own token

@@ -1,13 +1,14 @@
 // Token-wise decode entry point: one query per sequence against a paged KV cache.
 //
 // One kernel: workgroup = (256-key positional chunk, kv head, batch entry).
-// The G query heads of the kv head sit in the MFMA columns (padded to 32), so
+// The G query heads of the kv head sit in the MFMA columns (16 per block), so
 // each K/V tile is read from HBM once for the whole group.  The four waves
 // compute the same scores and softmax state (the shared per-tile sequence of
 // uattn_numerics.h) and each accumulates one 32-wide d block of the output.
 // A chunk's result is either final (the context fits in one chunk) or an
 // fp32 partial (m, l, acc) written to the workspace.  The page-table entries of
-// the chunk are fetched up front and two tiles are kept in flight.
+// the chunk are fetched up front; tiles move by direct-to-LDS loads into two
+// stages, the next tile loading while the current one is computed.
 //
 // Merge: the workgroup that completes an entry's last outstanding chunk
 // (an arrival counter per (entry, kv head), reset to zero after use) folds
@@ -78,11 +79,12 @@ __device__ __forceinline__ void merge_entry(const DecodeParams& p, int b, int kv
   }
 }
 
-template <int D>
+template <int D, int NB>
 __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * Lds<D>::kStageElems];
+  using TL = TileLayout<D>;
+  __shared__ __attribute__((aligned(1024))) __bf16 lds[2 * TL::kStageElems];
   __shared__ int s_last;
-  constexpr int NDB = D / 32;
+  constexpr int NDBW = D / 16 / 4;  // 16-wide d blocks of the output per wave
 
   const int chunk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int n = min(p.seqlens[b], p.max_seqlen);  // clamp (trusted) lengths to the sized grid
@@ -93,92 +95,112 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
   const int ntiles = min(kTilesPerChunk, last_tile - t0 + 1);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int h = lane >> 5, col = lane & 31;
+  const int g = lane >> 4, col = lane & 15;
   const int qpos = n - 1;
-  const int head = kvh * p.group + col;
 
-  // Where this thread's rows of each tile of the chunk live.  A thread's
-  // kKPU consecutive rows always share one page (pages are >= 16 keys).
-  const int r0 = TileIO<D>::first_row(tid);
+  // Where this wave's 16 rows of each tile of the chunk live (one page: pages
+  // hold >= 16 keys).  Looked up once, up front.
   const int32_t* bt_row = p.bt + static_cast<int64_t>(b) * p.maxp;
   int64_t off0[kTilesPerChunk];
   int nvalid[kTilesPerChunk];
 #pragma unroll
   for (int j = 0; j < kTilesPerChunk; ++j) {
-    const int pos = (t0 + j) * kTileKeys + r0;
+    const int pos = (t0 + j) * kTileKeys + 16 * wave;
     const int64_t page = (j < ntiles && pos < n) ? bt_row[pos / p.page_size] : -1;
     const bool ok = page >= 0 && page < p.num_pages;
     off0[j] = ok ? ((page * p.hkv + kvh) * p.page_size + (pos % p.page_size)) * D : 0;
     nvalid[j] = ok ? n - pos : 0;
   }
 
-  bf16x8 qf[D / 16];
-  if (col < p.group) {
-    const __bf16* qrow = p.q + (static_cast<int64_t>(b) * p.hq + head) * D + 8 * h;
+  // Q^T operands: the group's q heads in the MFMA columns (16 per block)
+  bf16x8 qf[NB][D / 32];
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st) qf[st] = *reinterpret_cast<const bf16x8*>(qrow + 16 * st);
-  } else {
+  for (int nb = 0; nb < NB; ++nb) {
+    const int gi = kQCols * nb + col;
+    if (gi < p.group) {
+      const __bf16* qrow = p.q + (static_cast<int64_t>(b) * p.hq + kvh * p.group + gi) * D + 8 * g;
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st)
+      for (int st = 0; st < D / 32; ++st) qf[nb][st] = *reinterpret_cast<const bf16x8*>(qrow + 32 * st);
+    } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qf[st][e] = static_cast<__bf16>(0.0f);
+      for (int st = 0; st < D / 32; ++st)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[nb][st][e] = static_cast<__bf16>(0.0f);
+    }
   }
 
-  // two tiles in flight in registers, two LDS stages
-  TileIO<D> io[2];
-  io[0].load(p.kp, p.vp, off0[0], D, nvalid[0], tid);
-  if (ntiles > 1) io[1].load(p.kp, p.vp, off0[1], D, nvalid[1], tid);
+  // two LDS stages: tile j+1 loads while tile j is computed
+  auto issue_tile = [&](int j) {
+    load_tile_rows<D, 16>(lds + (j & 1) * TL::kStageElems, p.kp + off0[j], p.vp + off0[j], D, nvalid[j], wave, lane);
+  };
+  issue_tile(0);
 
-  f32x16 acc[1];
+  f32x4 acc[NB][NDBW];
+  float m[NB], l[NB];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc[0][r] = 0.f;
-  float m = neg_inf(), l = 0.f;
+  for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+    for (int db = 0; db < NDBW; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m[nb] = neg_inf();
+    l[nb] = 0.f;
+  }
   const float c = p.c;
-  const bool pv_on = wave < NDB;
 
 #pragma unroll
   for (int j = 0; j < kTilesPerChunk; ++j) {
     if (j < ntiles) {
-      __bf16* stage = lds + (j & 1) * Lds<D>::kStageElems;
-      io[j & 1].store(stage, tid);
+      __bf16* stage = lds + (j & 1) * TL::kStageElems;
+      wait_tile_loads();
       __syncthreads();
-      if (j + 2 < ntiles) io[j & 1].load(p.kp, p.vp, off0[j + 2], D, nvalid[j + 2], tid);
+      if (j + 1 < ntiles) issue_tile(j + 1);
       const int t = t0 + j;
-      f32x16 s[2];
-      qk_scores<D>(stage, qf, s, lane);
-      if (t == last_tile) mask_scores(s, t * kTileKeys, qpos, lane);
-      const float alpha = softmax_tile(s, m, l, c);
-      bf16x8 pb[4];
-      pack_p(s, pb);
-      if (pv_on) pv_tile<D, 1>(stage + Lds<D>::kKElems, pb, acc, alpha, wave, lane);
+      f32x4 s[NB][4];
+      qk_scores<D, NB>(stage, qf, s, lane);
+      float alpha[NB];
+      bf16x8 pb[NB][2];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        if (t == last_tile) mask_scores(s[nb], t * kTileKeys, qpos, lane);
+        alpha[nb] = softmax_tile(s[nb], m[nb], l[nb], c);
+        pack_p(s[nb], pb[nb]);
+      }
+      pv_tile<D, NB, NDBW>(stage, pb, acc, alpha, wave * NDBW, lane);
     }
   }
 
   if (nch == 1) {
-    if (!pv_on || col >= p.group) return;
-    __bf16* orow = p.out + (static_cast<int64_t>(b) * p.hq + head) * D + 32 * wave;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      bf16x4 w;
+    for (int nb = 0; nb < NB; ++nb) {
+      const int gi = kQCols * nb + col;
+      if (gi >= p.group) continue;
+      const int64_t orow = (static_cast<int64_t>(b) * p.hq + kvh * p.group + gi);
+      __bf16* o = p.out + orow * D + 16 * wave * NDBW + 4 * g;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) w[j] = finalize_val(acc[0][4 * i + j], l);
-      *reinterpret_cast<bf16x4*>(orow + 8 * i + 4 * h) = w;
+      for (int db = 0; db < NDBW; ++db) {
+        bf16x4 w;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) w[jj] = finalize_val(acc[nb][db][jj], l[nb]);
+        *reinterpret_cast<bf16x4*>(o + 16 * db) = w;
+      }
+      if (p.lse != nullptr && wave == 0 && g == 0) p.lse[orow] = finalize_lse(m[nb], l[nb], c);
     }
-    if (p.lse != nullptr && wave == 0 && h == 0) p.lse[static_cast<int64_t>(b) * p.hq + head] = finalize_lse(m, l, c);
     return;
   }
 
   // chunk partial -> workspace
-  if (pv_on && col < p.group) {
-    const int64_t slot = (static_cast<int64_t>(b) * p.hq + head) * p.nchunk_max + chunk;
-    float* arow = p.ws_acc + slot * D + 32 * wave;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+  for (int nb = 0; nb < NB; ++nb) {
+    const int gi = kQCols * nb + col;
+    if (gi >= p.group) continue;
+    const int64_t slot = (static_cast<int64_t>(b) * p.hq + kvh * p.group + gi) * p.nchunk_max + chunk;
+    float* arow = p.ws_acc + slot * D + 16 * wave * NDBW + 4 * g;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) st_coherent(arow + 8 * i + 4 * h + j, acc[0][4 * i + j]);
-    if (wave == 0 && h == 0) {
-      st_coherent(p.ws_ml + slot * 2, m);
-      st_coherent(p.ws_ml + slot * 2 + 1, l);
+    for (int db = 0; db < NDBW; ++db)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) st_coherent(arow + 16 * db + jj, acc[nb][db][jj]);
+    if (wave == 0 && g == 0) {
+      st_coherent(p.ws_ml + slot * 2, m[nb]);
+      st_coherent(p.ws_ml + slot * 2 + 1, l[nb]);
     }
   }
   // The workgroup that completes the entry's last outstanding chunk folds
@@ -234,10 +256,18 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
   p.nchunk_max = a.nchunk_max;
   p.c = a.c;
   const dim3 grid(a.nchunk_max, a.num_kv_heads, a.batch);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(decode_kernel<128>, grid, dim3(256), 0, stream, p);
-  else
-    hipLaunchKernelGGL(decode_kernel<64>, grid, dim3(256), 0, stream, p);
+  const bool two = p.group > kQCols;
+  if (a.head_dim == 128) {
+    if (two)
+      hipLaunchKernelGGL((decode_kernel<128, 2>), grid, dim3(256), 0, stream, p);
+    else
+      hipLaunchKernelGGL((decode_kernel<128, 1>), grid, dim3(256), 0, stream, p);
+  } else {
+    if (two)
+      hipLaunchKernelGGL((decode_kernel<64, 2>), grid, dim3(256), 0, stream, p);
+    else
+      hipLaunchKernelGGL((decode_kernel<64, 1>), grid, dim3(256), 0, stream, p);
+  }
   return hipGetLastError();
 }
 

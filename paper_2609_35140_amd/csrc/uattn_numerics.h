@@ -18,16 +18,17 @@
 //     from (m = -inf, l = 0, acc = 0) and chunk results are folded left to
 //     right, whether or not the caller's schedule runs chunks in parallel;
 //   * scores S^T = K Q^T and the output O^T = V^T P^T are products on
-//     v_mfma_f32_32x32x16_bf16, with queries in the N (column) slots, d and
-//     keys consumed in fixed ascending 16-wide K steps starting from zero
+//     v_mfma_f32_16x16x32_bf16, with queries in the N (column) slots, d and
+//     keys consumed in fixed ascending 32-wide K steps starting from zero
 //     (scores) or from the rescaled accumulator (output);
 //   * the mask is a select to -inf (keys after the query), never a bias;
 //   * softmax runs on raw scores with the scale folded into the exponent:
 //     p = exp2(fma(s, c, -m*c)) with c = fp32(scale * log2(e)) computed once
 //     on the host; alpha = exp2(m_old*c - m_new*c); the hardware v_exp_f32;
-//   * l accumulates the fp32 p (in-lane pairwise tree, then the partner
-//     half-wave), acc is rescaled by alpha BEFORE the PV product accumulates
-//     into it, p is rounded to bf16 (nearest-even) only for the PV product;
+//   * l accumulates the fp32 p in one fixed tree (in-lane, then the lane
+//     groups holding the same column), acc is rescaled by alpha BEFORE the
+//     PV product accumulates into it, p is rounded to bf16 (nearest-even)
+//     only for the PV product;
 //   * no data-dependent skip of any multiply (alpha == 1 included);
 //     subnormals are preserved (the kernels' default fp32 denormal mode);
 //   * the result is bf16_rne(A / L) with IEEE division.
@@ -47,25 +48,41 @@ namespace uattn {
 constexpr int kTileKeys = 64;
 constexpr int kChunkKeys = 256;
 constexpr int kTilesPerChunk = kChunkKeys / kTileKeys;
-constexpr int kQCols = 32;  // query columns per MFMA (N of 32x32x16)
+constexpr int kQCols = 16;   // query columns per MFMA (N of 16x16x32)
+constexpr int kKeyBlocks = kTileKeys / 16;  // 16-key M blocks of a score tile
+constexpr int kMaxGroup = 2 * kQCols;       // q heads per kv head the decode kernel serves
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-// LDS row strides (elements).  K tile: [64 keys][D + 8]; V tile: [64 keys][kVStride].
-// Both tiles are stored key-major as they come from memory.  The K pad keeps
-// 16-lane groups of 128-bit reads on distinct banks; the V stride keeps the
-// 32-lane groups of transposing 64-bit reads (see pv_tile) on distinct banks.
-template <int D> struct Lds {
-  static constexpr int kKStride = D + 8;
-  static constexpr int kVStride = D == 128 ? 160 : 96;
-  static constexpr int kKElems = kTileKeys * kKStride;
-  static constexpr int kVElems = kTileKeys * kVStride;
-  static constexpr int kStageElems = kKElems + kVElems;
+// LDS layout of one pipeline stage: a K tile then a V tile, each [64 keys][D]
+// key-major as in memory, with the 16-byte pieces of every row permuted by an
+// XOR swizzle so that the two read patterns below hit distinct banks.
+template <int D>
+struct TileLayout {
+  static constexpr int kPieces = D / 8;                  // 16-byte pieces per row
+  static constexpr int kTileElems = kTileKeys * D;       // one K or V tile
+  static constexpr int kStageElems = 2 * kTileElems;     // K tile then V tile
+  static constexpr int kInstrPerWave = kPieces / 4;      // 1 KB instructions per wave per matrix
+
+  // K is read as 16 consecutive rows at one logical piece (16-lane groups of
+  // 128-bit reads): spread those rows over 16 distinct bank groups.
+  __device__ __forceinline__ static int k_swz(int row) { return D == 128 ? (row & 15) : ((row >> 1) & 7); }
+  // V is read by the transposing 64-bit read: 8 consecutive rows x 2 logical
+  // pieces (x 2 halves) per 32-lane group.
+  __device__ __forceinline__ static int v_swz(int row) { return D == 128 ? 2 * (row & 7) : 2 * ((row >> 1) & 3); }
+
+  // Element offsets inside a stage of (row, d) for K and V.
+  __device__ __forceinline__ static int k_off(int row, int d) {
+    return row * D + 8 * ((d >> 3) ^ k_swz(row)) + (d & 7);
+  }
+  __device__ __forceinline__ static int v_off(int row, int d) {
+    return kTileElems + row * D + 8 * ((d >> 3) ^ v_swz(row)) + (d & 7);
+  }
 };
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
@@ -75,135 +92,143 @@ __device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf
 
 __device__ __forceinline__ __bf16 to_bf16(float x) { return static_cast<__bf16>(x); }
 
-// ---------------------------------------------------------------------------
-// Register <-> key maps of the score tile.
-//
-// The 32x32 MFMA result holds, in lane half h = lane / 32, register r, the row
-// 8*(r/4) + 4*h + r%4 of the 32-row block.  Rows are keys; which key each
-// A-operand row carries is chosen so that, after the in-lane regrouping of
-// p into the PV operand, every 8 consecutive K slots of the PV product are 8
-// consecutive keys (two transposing reads of the V tile, 4 keys each).
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ constexpr int score_key(int blk, int r, int h) {
-  return 32 * blk + 16 * ((r >> 2) >> 1) + 8 * h + 4 * ((r >> 2) & 1) + (r & 3);
-}
-// Key carried by A-operand row `row` (0..31) of score block `blk`.
-__device__ __forceinline__ constexpr int arow_key(int blk, int row) {
-  return score_key(blk, ((row >> 3) << 2) | (row & 3), (row >> 2) & 1);
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
 // ---------------------------------------------------------------------------
-// Scores: s[blk] = K_blk Q^T over d, ascending 16-wide steps from zero.
-//   ks_lds : K tile in LDS, [64][Lds<D>::kKStride]
-//   qf     : this lane's Q^T operand, qf[step] = q[col][16*step + 8*h .. +7]
+// Layout of a score tile.  For one group of 16 queries (an N block), lane
+// L = 16*g + col holds query column `col` and, in s[kb][j], the score of key
+// 16*kb + 4*g + j of the 64-key tile (the 16x16 MFMA result layout: lane L,
+// register j holds row 4*(L/16) + j, column L%16).  The four lane groups g
+// of one column together hold its 64 keys.
 // ---------------------------------------------------------------------------
-template <int D>
-__device__ __forceinline__ void qk_scores(const __bf16* ks_lds, const bf16x8 (&qf)[D / 16], f32x16 (&s)[2], int lane) {
-  const int h = lane >> 5, row = lane & 31;
+__device__ __forceinline__ constexpr int score_key(int kb, int j, int g) { return 16 * kb + 4 * g + j; }
+
+// ---------------------------------------------------------------------------
+// Scores: s[nb][kb] = K_kb Q_nb^T over d in ascending 32-wide steps from zero.
+//   stage  : LDS stage holding the K tile (TileLayout)
+//   qf     : this lane's Q^T operands, qf[nb][step] = q[col of nb][32*step + 8*g .. +7]
+// ---------------------------------------------------------------------------
+template <int D, int NB>
+__device__ __forceinline__ void qk_scores(const __bf16* stage, const bf16x8 (&qf)[NB][D / 32], f32x4 (&s)[NB][4],
+                                          int lane) {
+  using TL = TileLayout<D>;
+  const int g = lane >> 4, row = lane & 15;
+  const int swz = TL::k_swz(row);  // equals k_swz(16*kb + row) for every kb
 #pragma unroll
-  for (int blk = 0; blk < 2; ++blk) {
-    const __bf16* krow = ks_lds + arow_key(blk, row) * Lds<D>::kKStride + 8 * h;
-    f32x16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int kb = 0; kb < kKeyBlocks; ++kb) {
+    const __bf16* krow = stage + (16 * kb + row) * D;
+    bf16x8 a[D / 32];
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + 16 * st);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], acc, 0, 0, 0);
+    for (int st = 0; st < D / 32; ++st) a[st] = *reinterpret_cast<const bf16x8*>(krow + 8 * ((4 * st + g) ^ swz));
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < D / 32; ++st) acc = mfma16(a[st], qf[nb][st], acc);
+      s[nb][kb] = acc;
     }
-    s[blk] = acc;
   }
 }
 
 // Select -inf for keys after the query: key position key_base + key > qpos.
-__device__ __forceinline__ void mask_scores(f32x16 (&s)[2], int key_base, int qpos, int lane) {
-  const int h = lane >> 5;
+__device__ __forceinline__ void mask_scores(f32x4 (&s)[4], int key_base, int qpos, int lane) {
+  const int g = lane >> 4;
 #pragma unroll
-  for (int blk = 0; blk < 2; ++blk)
+  for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      s[blk][r] = (key_base + score_key(blk, r, h) > qpos) ? neg_inf() : s[blk][r];
+    for (int j = 0; j < 4; ++j) s[kb][j] = (key_base + score_key(kb, j, g) > qpos) ? neg_inf() : s[kb][j];
 }
 
-// Cross-half partner value (lane ^ 32).
-__device__ __forceinline__ float partner(float x) {
-  return __shfl_xor(x, 32, 64);
-}
+// Reduction partners: the other lane groups holding the same query column.
+__device__ __forceinline__ float xor16(float x) { return __shfl_xor(x, 16, 64); }
+__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
 
 // ---------------------------------------------------------------------------
-// Online-softmax step for one tile.  In: raw scores s (masked).  Out: s holds
-// p = exp2(fma(s, c, -m_new*c)); m, l updated; returns alpha.
+// Online-softmax step of one query column for one tile.  In: raw scores s
+// (masked).  Out: s holds p = exp2(fma(s, c, -m_new*c)); m, l updated;
+// returns alpha.  The row sum is the fixed tree
+//   ((p0+p1)+(p2+p3)) over key blocks per j, ((u0+u1)+(u2+u3)) over j,
+//   then + lane^16, then + lane^32 (each step commutative, so every lane of
+//   the column ends with the same value).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float softmax_tile(f32x16 (&s)[2], float& m, float& l, float c) {
-  // tile max (exact, order-free)
-  float t[16];
+__device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float& l, float c) {
+  float t[4];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) t[r] = fmaxf(s[0][r], s[1][r]);
-#pragma unroll
-  for (int w = 8; w >= 1; w >>= 1)
-#pragma unroll
-    for (int r = 0; r < w; ++r) t[r] = fmaxf(t[r], t[r + w]);
-  float tmax = fmaxf(t[0], partner(t[0]));
+  for (int j = 0; j < 4; ++j) t[j] = fmaxf(fmaxf(s[0][j], s[1][j]), fmaxf(s[2][j], s[3][j]));
+  float tmax = fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3]));
+  tmax = fmaxf(tmax, xor16(tmax));
+  tmax = fmaxf(tmax, xor32(tmax));
   const float m_new = fmaxf(m, tmax);
   const float mc_old = m * c;
   const float mc_new = m_new * c;
   const float alpha = hw_exp2(mc_old - mc_new);
 #pragma unroll
-  for (int blk = 0; blk < 2; ++blk)
+  for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s[blk][r] = hw_exp2(__builtin_fmaf(s[blk][r], c, -mc_new));
-  // row sum: pairwise tree over (blk0 r, blk1 r), then r halves, then partner
-  float u[16];
+    for (int j = 0; j < 4; ++j) s[kb][j] = hw_exp2(__builtin_fmaf(s[kb][j], c, -mc_new));
+  float u[4];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) u[r] = s[0][r] + s[1][r];
-#pragma unroll
-  for (int w = 8; w >= 1; w >>= 1)
-#pragma unroll
-    for (int r = 0; r < w; ++r) u[r] = u[r] + u[r + w];
-  const float rs = u[0] + partner(u[0]);
+  for (int j = 0; j < 4; ++j) u[j] = (s[0][j] + s[1][j]) + (s[2][j] + s[3][j]);
+  float rs = (u[0] + u[1]) + (u[2] + u[3]);
+  rs = rs + xor16(rs);
+  rs = rs + xor32(rs);
   l = alpha * l + rs;
   m = m_new;
   return alpha;
 }
 
-// p (fp32, score layout) -> bf16 PV B-operand: step st, element e holds the
-// key 16*st + 8*h + e.
-__device__ __forceinline__ void pack_p(const f32x16 (&p)[2], bf16x8 (&pb)[4]) {
+// p (fp32, score layout) -> bf16 PV B operand.  Step st covers keys
+// 32*st .. 32*st+31; in lane group g, element e holds key
+// 32*st + 16*(e/4) + 4*g + e%4, i.e. s[2*st + e/4][e%4].
+__device__ __forceinline__ void pack_p(const f32x4 (&p)[4], bf16x8 (&pb)[2]) {
 #pragma unroll
-  for (int st = 0; st < 4; ++st)
+  for (int st = 0; st < 2; ++st)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pb[st][e] = to_bf16(p[st >> 1][4 * (2 * (st & 1) + (e >> 2)) + (e & 3)]);
+    for (int e = 0; e < 8; ++e) pb[st][e] = to_bf16(p[2 * st + (e >> 2)][e & 3]);
 }
 
-// acc[db] (O^T block db0+db: rows d, cols queries) <- alpha*acc + V^T_db P^T.
-//   vs_lds : V tile in LDS, key-major [64][Lds<D>::kVStride]
-// The A operand (row d, K slots = keys 16*st + 8*h + e) is gathered with the
-// transposing 64-bit LDS read: within each 16-lane group, lane 4a+b receives
-// element b of the 4-element rows addressed by lanes a, a+4, a+8, a+12.  So
-// source lane s addresses key (base + s/4) at column (group's d base + 4*(s%4)),
-// and lane i of the group receives column d base + i for four consecutive keys.
-typedef short s16x4 __attribute__((ext_vector_type(4)));
+// Transposing 64-bit LDS read (16-bit elements): within each 16-lane group,
+// lane 4a+b receives element b of the 4-element rows addressed by lanes a,
+// a+4, a+8, a+12.
 __device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
-template <int D, int NDB>
-__device__ __forceinline__ void pv_tile(const __bf16* vs_lds, const bf16x8 (&pb)[4], f32x16 (&acc)[NDB], float alpha,
-                                        int db0, int lane) {
-  const int g = lane >> 4, s = lane & 15;
-  const int h = g >> 1;
-  const int key0 = 8 * h + (s >> 2);
-  const int col0 = 16 * (g & 1) + 4 * (s & 3);
+
+// acc[nb][db] (O^T block: rows d = 16*(db0+db) + 4*g + j, column = query of nb)
+//   <- alpha[nb] * acc + V^T_db P_nb^T, K steps st = 0, 1 in order.
+//   stage  : LDS stage holding the V tile (TileLayout)
+// The V^T operand of step st for d block db (lane i of group g: row d = 16*db + i,
+// keys 32*st + 16*h + 4*g + k for the two halves h) comes from two transposing
+// reads whose source lane s addresses key (32*st + 16*h + 4*g + s/4), column
+// 16*db + 4*(s%4).
+template <int D, int NB, int NDB>
+__device__ __forceinline__ void pv_tile(const __bf16* stage, const bf16x8 (&pb)[NB][2], f32x4 (&acc)[NB][NDB],
+                                        const float (&alpha)[NB], int db0, int lane) {
+  using TL = TileLayout<D>;
+  const int g = lane >> 4, src = lane & 15;
+  const int key = 4 * g + (src >> 2);       // + 32*st + 16*half; the swizzle depends on key bits below 16
+  const int swz = TL::v_swz(key);
+  const int sub = src & 3;                  // 4-column group inside the 16-wide d block
+  const __bf16* vrow = stage + TL::kTileElems + key * D + 4 * (sub & 1);
 #pragma unroll
   for (int db = 0; db < NDB; ++db) {
+    const int piece = (2 * (db0 + db) + (sub >> 1)) ^ swz;
+    bf16x8 a[2];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[db][r] = alpha * acc[db][r];
-    const __bf16* vb = vs_lds + key0 * Lds<D>::kVStride + 32 * (db0 + db) + col0;
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      const s16x4 lo = lds_read_tr16(vb + (16 * st) * Lds<D>::kVStride);
-      const s16x4 hi = lds_read_tr16(vb + (16 * st + 4) * Lds<D>::kVStride);
+    for (int st = 0; st < 2; ++st) {
+      const s16x4 lo = lds_read_tr16(vrow + (32 * st) * D + 8 * piece);
+      const s16x4 hi = lds_read_tr16(vrow + (32 * st + 16) * D + 8 * piece);
       const s16x4 w[2] = {lo, hi};
-      bf16x8 a;
-      __builtin_memcpy(&a, w, sizeof(a));
-      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[st], acc[db], 0, 0, 0);
+      __builtin_memcpy(&a[st], w, sizeof(bf16x8));
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[nb][db][j] = alpha[nb] * acc[nb][db][j];
+#pragma unroll
+      for (int st = 0; st < 2; ++st) acc[nb][db] = mfma16(a[st], pb[nb][st], acc[nb][db]);
     }
   }
 }

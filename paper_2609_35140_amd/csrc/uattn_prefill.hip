@@ -1,16 +1,18 @@
 // Full-sequence entry point: causal GQA attention over a packed varlen batch.
 //
-// Workgroup = 4 waves = 128 consecutive query rows of one q head of one
-// sequence; wave w owns rows q0 .. q0+31 (q0 = tile*128 + 32*w), one row per
-// MFMA column.  All four waves stream the same K/V tiles through a double-
-// buffered LDS stage; a wave stops at its own diagonal tile (q0 / 64), so no
-// row ever sees a tile without a visible key.  Every row's arithmetic is the
-// shared per-tile sequence in uattn_numerics.h, chunk-folded every 4 tiles,
-// exactly as the decode path folds its positional split.
+// Workgroup = 8 waves = 128 consecutive query rows of one q head of one
+// sequence; wave w owns rows q0 .. q0+15 (q0 = tile*128 + 16*w), one row per
+// MFMA column.  Two waves share each SIMD, so one wave's matrix work overlaps
+// the other's softmax.  All waves stream the same K/V tiles through LDS
+// stages filled by direct-to-LDS loads; a wave stops at its own diagonal tile
+// (q0 / 64), so no row ever sees a tile without a visible key.  Every row's
+// arithmetic is the shared per-tile sequence in uattn_numerics.h,
+// chunk-folded every 4 tiles, exactly as the decode path folds its
+// positional split.
 //
-// Grid: x = q head, y = sequence, z = query tile counted from the END of the
-// sequence (z = 0 is the last, most expensive tile), so the longest work is
-// dispatched first.
+// Grid: one dimension; see the workgroup-id mapping below (query tiles counted
+// from the END of each sequence, so the longest work is dispatched first, and
+// the q heads sharing a kv head kept on one XCD).
 #include "uattn_internal.h"
 #include "uattn_numerics.h"
 #include "uattn_tile_io.h"
@@ -18,8 +20,20 @@
 namespace uattn {
 namespace {
 
-constexpr int kWaveRows = 32;
-constexpr int kWgRows = 128;
+#ifndef UATTN_PREFILL_WAVES
+#define UATTN_PREFILL_WAVES 8
+#endif
+constexpr int kWaves = UATTN_PREFILL_WAVES;
+#ifndef UATTN_PREFILL_NB
+#define UATTN_PREFILL_NB 2
+#endif
+constexpr int kNB = UATTN_PREFILL_NB;        // 16-column MFMA blocks (query groups) per wave
+constexpr int kWaveRows = kNB * kQCols;
+constexpr int kWgRows = kWaves * kWaveRows;
+#ifndef UATTN_PREFILL_STAGES
+#define UATTN_PREFILL_STAGES 2
+#endif
+constexpr int kStages = UATTN_PREFILL_STAGES;  // LDS ring: tiles are issued kStages-1 ahead
 
 struct PrefillParams {
   const __bf16* q;
@@ -29,115 +43,150 @@ struct PrefillParams {
   __bf16* out;
   float* lse;
   int hq, hkv, group, total;
+  int num_seqs, ngroups;  // work groups = (query tile from the end, sequence, kv head)
   float c;
 };
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillParams p) {
-  constexpr int NDB = D / 32;
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * Lds<D>::kStageElems];
+// Hardware dispatch hands consecutive workgroup ids to the 8 XCDs in turn, and
+// each XCD has its own L2.  Workgroup id -> (work group, q head in group) so
+// that the G q heads of one (tile, sequence, kv head), which read the same K/V
+// tiles, run back to back on the same XCD, while work groups are spread over
+// XCDs in descending-cost order (query tiles counted from the end first).
+constexpr int kXcds = 8;
 
-  const int head = blockIdx.x, seq = blockIdx.y;
+template <int D>
+__global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(PrefillParams p) {
+  constexpr int NDB = D / 16;  // 16-wide d blocks of the output
+  using TL = TileLayout<D>;
+  __shared__ __attribute__((aligned(1024))) __bf16 lds[kStages * TL::kStageElems];
+
+  const int pid = blockIdx.x;
+  const int k = pid / kXcds, gi = k % p.group;
+  const int wgroup = (k / p.group) * kXcds + pid % kXcds;
+  if (wgroup >= p.ngroups) return;
+  const int per_tile = p.num_seqs * p.hkv;
+  const int zrev = wgroup / per_tile;
+  const int seq = (wgroup % per_tile) / p.hkv;
+  const int kvh = wgroup % p.hkv;
+  const int head = kvh * p.group + gi;
   // clamp the (trusted) offsets so that a malformed table cannot index outside the tensors
   const int lo = min(max(p.cu[seq], 0), p.total);
   const int L = max(min(p.cu[seq + 1], p.total) - lo, 0);
   const int nqt = (L + kWgRows - 1) / kWgRows;
-  const int qt = nqt - 1 - static_cast<int>(blockIdx.z);
+  const int qt = nqt - 1 - zrev;
   if (qt < 0) return;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int h = lane >> 5, col = lane & 31;
+  const int g = lane >> 4, col = lane & 15;
   const int q0 = qt * kWgRows + wave * kWaveRows;
   const bool wave_on = q0 < L;
-  const int qpos = q0 + col;
-  const int kvh = head / p.group;
   const int last_q0 = min(qt * kWgRows + kWgRows - kWaveRows, ((L - 1) / kWaveRows) * kWaveRows);
   const int wg_last_tile = last_q0 / kTileKeys;
   const int my_last_tile = q0 / kTileKeys;
 
-  // this lane's Q^T operand
-  bf16x8 qf[D / 16];
-  if (wave_on && qpos < L) {
-    const __bf16* qrow = p.q + (static_cast<int64_t>(lo + qpos) * p.hq + head) * D + 8 * h;
+  // this lane's Q^T operands: query q0 + 16*nb + col, d = 32*step + 8*g .. +7
+  bf16x8 qf[kNB][D / 32];
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st) qf[st] = *reinterpret_cast<const bf16x8*>(qrow + 16 * st);
-  } else {
+  for (int nb = 0; nb < kNB; ++nb) {
+    const int qp = q0 + kQCols * nb + col;
+    if (wave_on && qp < L) {
+      const __bf16* qrow = p.q + (static_cast<int64_t>(lo + qp) * p.hq + head) * D + 8 * g;
 #pragma unroll
-    for (int st = 0; st < D / 16; ++st)
+      for (int st = 0; st < D / 32; ++st) qf[nb][st] = *reinterpret_cast<const bf16x8*>(qrow + 32 * st);
+    } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qf[st][e] = static_cast<__bf16>(0.0f);
+      for (int st = 0; st < D / 32; ++st)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[nb][st][e] = static_cast<__bf16>(0.0f);
+    }
   }
 
-  TileIO<D> io;
-  const int r0 = TileIO<D>::first_row(tid);
+  constexpr int RPW = kTileKeys / kWaves;
   const int64_t row_stride = static_cast<int64_t>(p.hkv) * D;
-  auto load_tile = [&](int t) {
-    const int pos = t * kTileKeys + r0;
-    io.load(p.k, p.v, (static_cast<int64_t>(lo + pos) * p.hkv + kvh) * D, row_stride, L - pos, tid);
+  auto issue_tile = [&](int t) {  // this wave's rows of tile t into stage t % kStages
+    const int pos = t * kTileKeys + RPW * wave;
+    const int64_t off = (static_cast<int64_t>(lo + pos) * p.hkv + kvh) * D;
+    load_tile_rows<D, RPW>(lds + (t % kStages) * TL::kStageElems, p.k + off, p.v + off, row_stride, L - pos, wave,
+                           lane);
   };
 
-  f32x16 acc[NDB], A[NDB];
+  f32x4 acc[kNB][NDB], A[kNB][NDB];
+  float m[kNB], l[kNB], M[kNB], Ls[kNB];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int nb = 0; nb < kNB; ++nb) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      acc[db][r] = 0.f;
-      A[db][r] = 0.f;
+    for (int db = 0; db < NDB; ++db) {
+      acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+      A[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-  float m = neg_inf(), l = 0.f, M = neg_inf(), Ls = 0.f;
+    m[nb] = neg_inf();
+    l[nb] = 0.f;
+    M[nb] = neg_inf();
+    Ls[nb] = 0.f;
+  }
   const float c = p.c;
 
-  load_tile(0);
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t)
+    if (t <= wg_last_tile) issue_tile(t);
   for (int t = 0; t <= wg_last_tile; ++t) {
-    __bf16* stage = lds + (t & 1) * Lds<D>::kStageElems;
-    io.store(stage, tid);
-    __syncthreads();
-    if (t < wg_last_tile) load_tile(t + 1);
+    __bf16* stage = lds + (t % kStages) * TL::kStageElems;
+    // this wave's rows of tile t are in LDS once only the later tiles' loads remain
+    wait_tiles_pending<TileLoads<D, RPW>::kPerTile>(min(kStages - 2, wg_last_tile - t));
+    __syncthreads();  // every wave's rows are, and every wave is done with tile t-1
+    if (t + kStages - 1 <= wg_last_tile) issue_tile(t + kStages - 1);
     if (wave_on && t <= my_last_tile) {
-      f32x16 s[2];
-      qk_scores<D>(stage, qf, s, lane);
-      if (t == my_last_tile) mask_scores(s, t * kTileKeys, qpos, lane);
-      const float alpha = softmax_tile(s, m, l, c);
-      bf16x8 pb[4];
-      pack_p(s, pb);
-      pv_tile<D, NDB>(stage + Lds<D>::kKElems, pb, acc, alpha, 0, lane);
+      f32x4 s[kNB][4];
+      qk_scores<D, kNB>(stage, qf, s, lane);
+      float alpha[kNB];
+      bf16x8 pb[kNB][2];
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) {
+        if (t == my_last_tile) mask_scores(s[nb], t * kTileKeys, q0 + kQCols * nb + col, lane);
+        alpha[nb] = softmax_tile(s[nb], m[nb], l[nb], c);
+        pack_p(s[nb], pb[nb]);
+      }
+      pv_tile<D, kNB, NDB>(stage, pb, acc, alpha, 0, lane);
       if (t == my_last_tile || (t % kTilesPerChunk) == kTilesPerChunk - 1) {
-        if (t < kTilesPerChunk) {
-          M = m;
-          Ls = l;
 #pragma unroll
-          for (int db = 0; db < NDB; ++db) A[db] = acc[db];
-        } else {
-          const FoldScale f = fold_scale(M, m, c);
-          Ls = fold_val(f, Ls, l);
+        for (int nb = 0; nb < kNB; ++nb) {
+          if (t < kTilesPerChunk) {
+            M[nb] = m[nb];
+            Ls[nb] = l[nb];
 #pragma unroll
-          for (int db = 0; db < NDB; ++db)
+            for (int db = 0; db < NDB; ++db) A[nb][db] = acc[nb][db];
+          } else {
+            const FoldScale f = fold_scale(M[nb], m[nb], c);
+            Ls[nb] = fold_val(f, Ls[nb], l[nb]);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) A[db][r] = fold_val(f, A[db][r], acc[db][r]);
-          M = f.m_new;
+            for (int db = 0; db < NDB; ++db)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) A[nb][db][j] = fold_val(f, A[nb][db][j], acc[nb][db][j]);
+            M[nb] = f.m_new;
+          }
+          m[nb] = neg_inf();
+          l[nb] = 0.f;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        m = neg_inf();
-        l = 0.f;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
       }
     }
   }
 
-  if (wave_on && qpos < L) {
-    __bf16* orow = p.out + (static_cast<int64_t>(lo + qpos) * p.hq + head) * D;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+  for (int nb = 0; nb < kNB; ++nb) {
+    const int qp = q0 + kQCols * nb + col;
+    if (wave_on && qp < L) {
+      __bf16* orow = p.out + (static_cast<int64_t>(lo + qp) * p.hq + head) * D + 4 * g;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int db = 0; db < NDB; ++db) {
         bf16x4 w;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = finalize_val(A[db][4 * i + j], Ls);
-        *reinterpret_cast<bf16x4*>(orow + 32 * db + 8 * i + 4 * h) = w;
+        for (int j = 0; j < 4; ++j) w[j] = finalize_val(A[nb][db][j], Ls[nb]);
+        *reinterpret_cast<bf16x4*>(orow + 16 * db) = w;
       }
-    if (p.lse != nullptr && h == 0) p.lse[static_cast<int64_t>(lo + qpos) * p.hq + head] = finalize_lse(M, Ls, c);
+      if (p.lse != nullptr && g == 0) p.lse[static_cast<int64_t>(lo + qp) * p.hq + head] = finalize_lse(M[nb], Ls[nb], c);
+    }
   }
 }
 
@@ -156,8 +205,14 @@ hipError_t launch_prefill(const PrefillLaunch& a, hipStream_t stream) {
   p.group = a.num_q_heads / a.num_kv_heads;
   p.total = a.total_tokens;
   p.c = a.c;
-  const dim3 grid(a.num_q_heads, a.num_seqs, (a.max_seqlen + kWgRows - 1) / kWgRows);
-  const dim3 block(256);
+  p.num_seqs = a.num_seqs;
+  const int64_t ntiles = (a.max_seqlen + kWgRows - 1) / kWgRows;
+  const int64_t ngroups = ntiles * a.num_seqs * a.num_kv_heads;
+  const int64_t nblocks = (ngroups + kXcds - 1) / kXcds * kXcds * p.group;
+  if (nblocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+  p.ngroups = static_cast<int>(ngroups);
+  const dim3 grid(static_cast<unsigned>(nblocks));
+  const dim3 block(kWaves * 64);
   if (a.head_dim == 128)
     hipLaunchKernelGGL(prefill_kernel<128>, grid, block, 0, stream, p);
   else

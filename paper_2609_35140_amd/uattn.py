@@ -13,7 +13,7 @@ import os
 from typing import Optional, Tuple
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libuattn.so")
+LIB_PATH = os.environ.get("UATTN_LIB") or os.path.join(_PKG, "libuattn.so")
 
 UATTN_OK = 0
 TILE_KEYS = 64
