@@ -9,6 +9,7 @@ the HIP kernels or the binding, and neither imports the other.
 """
 from .attention import (  # noqa: F401
     CHUNK_KEYS,
+    LSE_ABS,
     TILE_KEYS,
     attention_row_fp64,
     attention_rows_fp64,

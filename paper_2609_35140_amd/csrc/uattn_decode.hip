@@ -135,14 +135,14 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
   };
   issue_tile(0);
 
-  f32x4 acc[NB][NDBW];
-  float m[NB], l[NB];
+  f32x4 acc[NB][NDBW], lsum[NB];
+  float m[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
     for (int db = 0; db < NDBW; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     m[nb] = neg_inf();
-    l[nb] = 0.f;
+    lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   const float c = p.c;
 
@@ -161,10 +161,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         if (t == last_tile) mask_scores(s[nb], t * kTileKeys, qpos, lane);
-        alpha[nb] = softmax_tile(s[nb], m[nb], l[nb], c);
+        alpha[nb] = softmax_tile(s[nb], m[nb], c);
         pack_p(s[nb], pb[nb]);
       }
-      pv_tile<D, NB, NDBW>(stage, pb, acc, alpha, wave * NDBW, lane);
+      pv_tile<D, NB, NDBW>(stage, pb, acc, lsum, alpha, wave * NDBW, lane);
     }
   }
 
@@ -179,10 +179,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
       for (int db = 0; db < NDBW; ++db) {
         bf16x4 w;
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) w[jj] = finalize_val(acc[nb][db][jj], l[nb]);
+        for (int jj = 0; jj < 4; ++jj) w[jj] = finalize_val(acc[nb][db][jj], lsum[nb][0]);
         *reinterpret_cast<bf16x4*>(o + 16 * db) = w;
       }
-      if (p.lse != nullptr && wave == 0 && g == 0) p.lse[orow] = finalize_lse(m[nb], l[nb], c);
+      if (p.lse != nullptr && wave == 0 && g == 0) p.lse[orow] = finalize_lse(m[nb], lsum[nb][0], c);
     }
     return;
   }
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
       for (int jj = 0; jj < 4; ++jj) st_coherent(arow + 16 * db + jj, acc[nb][db][jj]);
     if (wave == 0 && g == 0) {
       st_coherent(p.ws_ml + slot * 2, m[nb]);
-      st_coherent(p.ws_ml + slot * 2 + 1, l[nb]);
+      st_coherent(p.ws_ml + slot * 2 + 1, lsum[nb][0]);
     }
   }
   // The workgroup that completes the entry's last outstanding chunk folds

@@ -25,10 +25,10 @@
 //   * softmax runs on raw scores with the scale folded into the exponent:
 //     p = exp2(fma(s, c, -m*c)) with c = fp32(scale * log2(e)) computed once
 //     on the host; alpha = exp2(m_old*c - m_new*c); the hardware v_exp_f32;
-//   * l accumulates the fp32 p in one fixed tree (in-lane, then the lane
-//     groups holding the same column), acc is rescaled by alpha BEFORE the
-//     PV product accumulates into it, p is rounded to bf16 (nearest-even)
-//     only for the PV product;
+//   * p is rounded to bf16 (nearest-even) for the PV product, and l is the
+//     sum of the same bf16 p, accumulated by that product (an extra all-ones
+//     row block); acc and l are rescaled by alpha BEFORE the product
+//     accumulates into them;
 //   * no data-dependent skip of any multiply (alpha == 1 included);
 //     subnormals are preserved (the kernels' default fp32 denormal mode);
 //   * the result is bf16_rne(A / L) with IEEE division.
@@ -141,25 +141,34 @@ __device__ __forceinline__ void mask_scores(f32x4 (&s)[4], int key_base, int qpo
     for (int j = 0; j < 4; ++j) s[kb][j] = (key_base + score_key(kb, j, g) > qpos) ? neg_inf() : s[kb][j];
 }
 
-// Reduction partners: the other lane groups holding the same query column.
-__device__ __forceinline__ float xor16(float x) { return __shfl_xor(x, 16, 64); }
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+// Cross-group reductions with the gfx950 lane-swap instructions.  With both
+// operands equal, permlane32_swap returns (lanes 0-31 copied to both halves,
+// lanes 32-63 copied to both halves) and permlane16_swap does the same for
+// the 16-lane halves of each 32-lane half, so combining the two results gives
+// every lane the reduction of itself and its lane^32 (lane^16) partner, with
+// the operands in the same order in every lane.
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 
 // ---------------------------------------------------------------------------
 // Online-softmax step of one query column for one tile.  In: raw scores s
-// (masked).  Out: s holds p = exp2(fma(s, c, -m_new*c)); m, l updated;
-// returns alpha.  The row sum is the fixed tree
-//   ((p0+p1)+(p2+p3)) over key blocks per j, ((u0+u1)+(u2+u3)) over j,
-//   then + lane^16, then + lane^32 (each step commutative, so every lane of
-//   the column ends with the same value).
+// (masked).  Out: s holds p = exp2(fma(s, c, -m_new*c)); m updated; returns
+// alpha = exp2(m_old*c - m_new*c).  The row sum l is accumulated by the PV
+// product (pv_tile), from the same bf16 p that weights V.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float& l, float c) {
+__device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float c) {
   float t[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) t[j] = fmaxf(fmaxf(s[0][j], s[1][j]), fmaxf(s[2][j], s[3][j]));
   float tmax = fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3]));
-  tmax = fmaxf(tmax, xor16(tmax));
-  tmax = fmaxf(tmax, xor32(tmax));
+  tmax = max_xor16(tmax);
+  tmax = max_xor32(tmax);
   const float m_new = fmaxf(m, tmax);
   const float mc_old = m * c;
   const float mc_new = m_new * c;
@@ -168,13 +177,6 @@ __device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float& l,
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
     for (int j = 0; j < 4; ++j) s[kb][j] = hw_exp2(__builtin_fmaf(s[kb][j], c, -mc_new));
-  float u[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) u[j] = (s[0][j] + s[1][j]) + (s[2][j] + s[3][j]);
-  float rs = (u[0] + u[1]) + (u[2] + u[3]);
-  rs = rs + xor16(rs);
-  rs = rs + xor32(rs);
-  l = alpha * l + rs;
   m = m_new;
   return alpha;
 }
@@ -197,7 +199,10 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
 }
 
 // acc[nb][db] (O^T block: rows d = 16*(db0+db) + 4*g + j, column = query of nb)
-//   <- alpha[nb] * acc + V^T_db P_nb^T, K steps st = 0, 1 in order.
+//   <- alpha[nb] * acc + V^T_db P_nb^T, K steps st = 0, 1 in order;
+// lsum[nb] <- alpha[nb] * lsum + 1^T P_nb^T: the same product with an all-ones
+// operand in place of V^T, so every register of lsum holds the column's
+// running sum of the bf16 weights (l).
 //   stage  : LDS stage holding the V tile (TileLayout)
 // The V^T operand of step st for d block db (lane i of group g: row d = 16*db + i,
 // keys 32*st + 16*h + 4*g + k for the two halves h) comes from two transposing
@@ -205,13 +210,23 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
 // 16*db + 4*(s%4).
 template <int D, int NB, int NDB>
 __device__ __forceinline__ void pv_tile(const __bf16* stage, const bf16x8 (&pb)[NB][2], f32x4 (&acc)[NB][NDB],
-                                        const float (&alpha)[NB], int db0, int lane) {
+                                        f32x4 (&lsum)[NB], const float (&alpha)[NB], int db0, int lane) {
   using TL = TileLayout<D>;
   const int g = lane >> 4, src = lane & 15;
   const int key = 4 * g + (src >> 2);       // + 32*st + 16*half; the swizzle depends on key bits below 16
   const int swz = TL::v_swz(key);
   const int sub = src & 3;                  // 4-column group inside the 16-wide d block
   const __bf16* vrow = stage + TL::kTileElems + key * D + 4 * (sub & 1);
+  bf16x8 ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) lsum[nb][j] = alpha[nb] * lsum[nb][j];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) lsum[nb] = mfma16(ones, pb[nb][st], lsum[nb]);
+  }
 #pragma unroll
   for (int db = 0; db < NDB; ++db) {
     const int piece = (2 * (db0 + db) + (sub >> 1)) ^ swz;

@@ -110,8 +110,8 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
                            lane);
   };
 
-  f32x4 acc[kNB][NDB], A[kNB][NDB];
-  float m[kNB], l[kNB], M[kNB], Ls[kNB];
+  f32x4 acc[kNB][NDB], A[kNB][NDB], lsum[kNB];
+  float m[kNB], M[kNB], Ls[kNB];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
 #pragma unroll
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
       A[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     m[nb] = neg_inf();
-    l[nb] = 0.f;
+    lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     M[nb] = neg_inf();
     Ls[nb] = 0.f;
   }
@@ -143,21 +143,21 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) {
         if (t == my_last_tile) mask_scores(s[nb], t * kTileKeys, q0 + kQCols * nb + col, lane);
-        alpha[nb] = softmax_tile(s[nb], m[nb], l[nb], c);
+        alpha[nb] = softmax_tile(s[nb], m[nb], c);
         pack_p(s[nb], pb[nb]);
       }
-      pv_tile<D, kNB, NDB>(stage, pb, acc, alpha, 0, lane);
+      pv_tile<D, kNB, NDB>(stage, pb, acc, lsum, alpha, 0, lane);
       if (t == my_last_tile || (t % kTilesPerChunk) == kTilesPerChunk - 1) {
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) {
           if (t < kTilesPerChunk) {
             M[nb] = m[nb];
-            Ls[nb] = l[nb];
+            Ls[nb] = lsum[nb][0];
 #pragma unroll
             for (int db = 0; db < NDB; ++db) A[nb][db] = acc[nb][db];
           } else {
             const FoldScale f = fold_scale(M[nb], m[nb], c);
-            Ls[nb] = fold_val(f, Ls[nb], l[nb]);
+            Ls[nb] = fold_val(f, Ls[nb], lsum[nb][0]);
 #pragma unroll
             for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
             M[nb] = f.m_new;
           }
           m[nb] = neg_inf();
-          l[nb] = 0.f;
+          lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int db = 0; db < NDB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
         }

@@ -55,7 +55,7 @@ def test_emulator_within_gate_tiny(seed):
     o32, lse32 = oracle.tile_emulate_fp32(t["q"], t["k"], t["v"], t["cu_seqlens"])
     rep = oracle.parity_report(o32, o64)
     assert rep["pass"], rep
-    assert np.max(np.abs(lse32 - lse64)) < 1e-4
+    assert np.max(np.abs(lse32 - lse64)) < oracle.LSE_ABS
 
 
 def test_emulator_multi_chunk_within_gate():
