@@ -37,6 +37,19 @@ bool copy_back(std::vector<T>& host, const T* dev, size_t n) {
 
 }  // namespace
 
+namespace uattn {
+int32_t device_cus() {
+  static int32_t cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  cached[dev] = n;
+  return n;
+}
+}  // namespace uattn
+
 extern "C" {
 
 int32_t uattn_abi_version(void) { return UATTN_ABI_VERSION; }
@@ -165,6 +178,7 @@ uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_page
   a.num_q_heads = num_q_heads;
   a.num_kv_heads = num_kv_heads;
   a.head_dim = head_dim;
+  a.num_cus = uattn::device_cus();
   a.c = exp2_scale(softmax_scale);
   return uattn::launch_decode(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
 }

@@ -43,6 +43,7 @@ struct DecodeLaunch {
   int32_t num_q_heads;
   int32_t num_kv_heads;
   int32_t head_dim;
+  int32_t num_cus;  // compute units of the current device (sizes the persistent grid)
   float c;
 };
 
@@ -55,6 +56,9 @@ struct LogprobLaunch {
   int32_t vocab;
   float inv_temperature;
 };
+
+// Compute units of the current device (cached per device; 256 if the query fails).
+int32_t device_cus();
 
 // Each returns hipSuccess or the launch error.
 hipError_t launch_prefill(const PrefillLaunch& a, hipStream_t stream);
