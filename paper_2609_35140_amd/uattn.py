@@ -268,7 +268,11 @@ class DecodeSteps:
     def __len__(self):
         return len(self.args)
 
-    def run(self, i: int):
-        code = self._fn(*self.args[i])
+    def run(self, i: int, stream=None):
+        """Launch step i (on ``stream`` if given, else the stream fixed at construction)."""
+        a = self.args[i]
+        if stream is not None:
+            a = a[:-1] + (_stream(stream),)
+        code = self._fn(*a)
         if code != UATTN_OK:
             raise UattnError(status_string(code))
