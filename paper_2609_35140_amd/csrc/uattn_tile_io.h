@@ -59,6 +59,88 @@ __device__ __forceinline__ void load_tile_rows(__bf16* stage, const __bf16* kbas
   }
 }
 
+// ---------------------------------------------------------------------------
+// Explicitly scheduled variant.  The compiler's wait-count pass cannot tell an
+// LDS read from an earlier direct-to-LDS load that writes other LDS bytes, so
+// with the builtin loads it drains every outstanding load before the first
+// transposing LDS read of a tile, and a plain __syncthreads() drains them too
+// (its workgroup release fence).  Both defeat loads kept in flight across
+// tiles.  The loads below are issued from inline assembly, which that pass
+// does not track; the caller then owns every vmcnt wait before reading what
+// they wrote, and synchronises the workgroup with lds_barrier / wait_barrier.
+// The compiler allocates nothing in M0 in the kernels that use these.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// LDS byte address of a generic pointer into LDS: the shared aperture is
+// 4 GB aligned, so it is the low 32 bits of the flat address (no address
+// space cast, whose null check the compiler may mishandle).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+// 16 bytes per lane from `src` to LDS at m0 + 16*lane (m0 wave-uniform).
+__device__ __forceinline__ void dma_b128(const void* src, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds_wave_base)
+               : "memory", "m0");
+}
+// 4 bytes per lane from `src` to LDS at m0 + 4*lane.
+__device__ __forceinline__ void dma_b32(const void* src, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(src), "s"(lds_wave_base)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Workgroup barrier that orders LDS only (no wait on global memory).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// Wait until at most n vector-memory operations of this wave are outstanding,
+// then barrier: every wave's loads issued before its last n have landed.
+template <int n>
+__device__ __forceinline__ void wait_barrier() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" : : "n"(n) : "memory");
+}
+template <int n>
+__device__ __forceinline__ void wait_vmem_asm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(n) : "memory");
+}
+// wait_barrier for the tile ring: all but the `pending` most recently issued
+// tiles (per_tile operations each) have landed, in every wave.
+template <int per_tile>
+__device__ __forceinline__ void wait_tiles_barrier(int pending) {
+  switch (pending) {
+    case 0: wait_barrier<0>(); break;
+    case 1: wait_barrier<per_tile>(); break;
+    case 2: wait_barrier<2 * per_tile>(); break;
+    default: wait_barrier<3 * per_tile>(); break;
+  }
+}
+
+// load_tile_rows with the untracked loads (same rows, pieces and swizzle).
+template <int D, int RPW>
+__device__ __forceinline__ void load_tile_rows_async(__bf16* stage, const __bf16* kbase, const __bf16* vbase,
+                                                     int64_t row_stride, int nvalid, int wave, int lane) {
+  using TL = TileLayout<D>;
+  constexpr int kInstr = RPW * TL::kPieces / 64;
+  static_assert(kInstr >= 1 && RPW * TL::kPieces == 64 * kInstr, "tile split");
+  const __bf16* zero = reinterpret_cast<const __bf16*>(g_zero_rows) + 8 * (lane & 15);
+  const uint32_t kd0 = __builtin_amdgcn_readfirstlane(lds_addr(stage + wave * kInstr * 64 * 8));
+#pragma unroll
+  for (int i = 0; i < kInstr; ++i) {
+    const int slot = (wave * kInstr + i) * 64 + lane;
+    const int row = slot / TL::kPieces, piece = slot % TL::kPieces;
+    const int r = row - RPW * wave;
+    const bool ok = r < nvalid;
+    const __bf16* ks = ok ? kbase + r * row_stride + 8 * (piece ^ TL::k_swz(row)) : zero;
+    const __bf16* vs = ok ? vbase + r * row_stride + 8 * (piece ^ TL::v_swz(row)) : zero;
+    dma_b128(ks, kd0 + i * 64 * 16);
+    dma_b128(vs, kd0 + i * 64 * 16 + TL::kTileElems * 2);
+  }
+}
+
 // Wait until at most `n` of this wave's vector-memory operations are still
 // outstanding (they complete in issue order, so every earlier load has landed).
 template <int n>
