@@ -106,8 +106,8 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
   auto issue_tile = [&](int t) {  // this wave's rows of tile t into stage t % kStages
     const int pos = t * kTileKeys + RPW * wave;
     const int64_t off = (static_cast<int64_t>(lo + pos) * p.hkv + kvh) * D;
-    load_tile_rows<D, RPW>(lds + (t % kStages) * TL::kStageElems, p.k + off, p.v + off, row_stride, L - pos, wave,
-                           lane);
+    load_tile_rows_async<D, RPW>(lds + (t % kStages) * TL::kStageElems, p.k + off, p.v + off, row_stride, L - pos,
+                                 wave, lane);
   };
 
   f32x4 acc[kNB][NDB], A[kNB][NDB], lsum[kNB];
@@ -131,9 +131,10 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
     if (t <= wg_last_tile) issue_tile(t);
   for (int t = 0; t <= wg_last_tile; ++t) {
     __bf16* stage = lds + (t % kStages) * TL::kStageElems;
-    // this wave's rows of tile t are in LDS once only the later tiles' loads remain
-    wait_tiles_pending<TileLoads<D, RPW>::kPerTile>(min(kStages - 2, wg_last_tile - t));
-    __syncthreads();  // every wave's rows are, and every wave is done with tile t-1
+    // this wave's rows of tile t are in LDS once only the later tiles' loads
+    // remain; after the barrier every wave's rows are, and every wave is done
+    // with tile t-1
+    wait_tiles_barrier<TileLoads<D, RPW>::kPerTile>(min(kStages - 2, wg_last_tile - t));
     if (t + kStages - 1 <= wg_last_tile) issue_tile(t + kStages - 1);
     if (wave_on && t <= my_last_tile) {
       f32x4 s[kNB][4];
