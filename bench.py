@@ -50,7 +50,43 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
     ap.add_argument("--eager-decode", action="store_true", help="launch the decode steps one by one (no HIP graph)")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="before timing, copy 1 GiB device to device once (the known-size dispatch that scales "
+                         "the FETCH_SIZE / WRITE_SIZE counters of a profiling run)")
     return ap.parse_args()
+
+
+DECODE_SOURCES = ("uattn_decode.hip", "uattn_numerics.h", "uattn_tile_io.h", "uattn_internal.h")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_kernel_qwen_gqa_traffic.md")
+
+
+def decode_source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in DECODE_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_35140_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter summary, or None
+    when it is absent or was taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            text = f.read()
+    except OSError:
+        return None
+    blk = text.split("```json", 1)
+    if len(blk) < 2:
+        return None
+    try:
+        rec = json.loads(blk[1].split("```", 1)[0])
+    except ValueError:
+        return None
+    if rec.get("source_sha256") != decode_source_digest():
+        return None
+    return rec
 
 
 class Ev:
@@ -67,8 +103,8 @@ class Ev:
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md for how it would "
-              "shard). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: there is no multi-GPU path (the kernels would shard by sequence or "
+              "kv head with no exchange). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -121,6 +157,15 @@ def main():
     logp = torch.empty(rows, dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
     log(f"inputs ready in {time.time() - t0:.1f}s: T={q.shape[0]} pages={npages} logits={tuple(logits.shape)}")
+    if args.calibration_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("calibration copy: 1 GiB device to device")
 
     # ------------------------------------------------------------------ one step
     # The 3072 token-wise decode launches run as one HIP graph (captured once,
@@ -211,6 +256,7 @@ def main():
 
     dec_launch_bytes = dec_bytes / R
     dec_launch_ms = dec_kernel_ms / R
+    traffic = measured_traffic()
     result = {
         "metric": METRIC,
         "value": round(dec_gbs_wall, 2),
@@ -240,7 +286,9 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(dec_launch_bytes / (dec_launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": traffic["hbm_bytes_per_launch"] if traffic else None,
+            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+            "traffic_over_algorithmic": round(traffic["hbm_bytes_per_launch"] / dec_launch_bytes, 4) if traffic else None,
             "bytes_per_launch": dec_launch_bytes,
             "avg_launch_ms": round(dec_launch_ms, 5),
             "avg_launch_ms_is": "decode-phase event time / 3072 launches (includes the graph's inter-launch gaps)",
