@@ -6,6 +6,7 @@ workload (8 sequences of 1024 prompt + 3072 response tokens, 32 q / 8 kv
 heads, head_dim 128, bf16 ~ N(0, 0.25), paged KV with 64-token pages):
 
   1. rollout prefill over the 8 prompts             (full-sequence entry point)
+     and the indexed write of the prompts' K/V into the paged cache
   2. rollout decode of the 3072 response tokens,
      token by token, batch 8, against the paged cache (token-wise entry point)
   3. policy-update prefill over the 8 full trajectories (full-sequence entry point)
@@ -56,7 +57,7 @@ def parse():
     return ap.parse_args()
 
 
-DECODE_SOURCES = ("uattn_decode.hip", "uattn_numerics.h", "uattn_tile_io.h", "uattn_internal.h")
+DECODE_SOURCES = ("uattn_decode.hip", "uattn_numerics.h", "uattn_tile_io.h")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_kernel_qwen_gqa_traffic.md")
 
 
@@ -142,6 +143,9 @@ def main():
     pidx = torch.from_numpy(np.concatenate([np.arange(cu[b], cu[b] + P) for b in range(B)])).to(dev)
     qp, kpk, vpk = q[pidx].contiguous(), k[pidx].contiguous(), v[pidx].contiguous()
     cu_p = torch.from_numpy(inputs.cu_seqlens([P] * B)).to(dev)
+    # the rollout writes the prompt's K/V into the paged cache (same bits the cache already holds)
+    seq_p = torch.from_numpy(np.repeat(np.arange(B, dtype=np.int32), P)).to(dev)
+    pos_p = torch.from_numpy(np.tile(np.arange(P, dtype=np.int32), B)).to(dev)
     # decode steps: query of token P+s of every sequence; context P+s+1
     tok = torch.from_numpy((cu[:B][None, :] + P + np.arange(R)[:, None]).astype(np.int64)).to(dev)  # [R, B]
     q_steps = q[tok.reshape(-1)].reshape(R, B, hq, d).contiguous()
@@ -185,6 +189,9 @@ def main():
         ev["pre"].a.record()
         uattn.prefill(qp, kpk, vpk, cu_p, P, out=out_prompt)
         ev["pre"].b.record()
+        ev["kvw"].a.record()
+        uattn.kv_write(kpk, vpk, table_dev, seq_p, pos_p, kp, vp)
+        ev["kvw"].b.record()
         ev["dec"].a.record()
         if graph is not None:
             graph.replay()
@@ -200,7 +207,7 @@ def main():
         ev["lp"].b.record()
 
     def new_events():
-        return {"pre": Ev(torch), "upd": Ev(torch), "lp": Ev(torch), "dec": Ev(torch)}
+        return {"pre": Ev(torch), "kvw": Ev(torch), "upd": Ev(torch), "lp": Ev(torch), "dec": Ev(torch)}
 
     for i in range(args.warmup):
         step(new_events())
@@ -219,6 +226,7 @@ def main():
     pre_ms = sum(e["pre"].ms() for e in evs) / K
     upd_ms = sum(e["upd"].ms() for e in evs) / K
     lp_ms = sum(e["lp"].ms() for e in evs) / K
+    kvw_ms = sum(e["kvw"].ms() for e in evs) / K
     dec_wall_ms = sum(e["dec"].ms() for e in evs) / K
     dec_kernel_ms = dec_wall_ms
     step_ms = wall / K * 1e3
@@ -231,6 +239,8 @@ def main():
     pre_tflops = pre_flop / (pre_ms * 1e-3) / 1e12
     dec_gbs_wall = dec_bytes / (dec_wall_ms * 1e-3) / 1e9
     lp_gbs = lp_bytes / (lp_ms * 1e-3) / 1e9
+    kvw_bytes = float(B * P) * hkv * d * 2 * 2 * 2      # K and V rows read once and written once
+    kvw_gbs = kvw_bytes / (kvw_ms * 1e-3) / 1e9
 
     # ------------------------------------------------------------------ bitwise Eq. (1)
     full_bits = out_full.view(torch.int16)
@@ -303,11 +313,13 @@ def main():
             "flop_per_launch": upd_flop,
             "avg_launch_ms": round(upd_ms, 4),
         },
-        "phases_ms": {"prompt_prefill": round(pre_ms, 4), "decode": round(dec_wall_ms, 3),
+        "phases_ms": {"prompt_prefill": round(pre_ms, 4), "kv_write": round(kvw_ms, 4), "decode": round(dec_wall_ms, 3),
                       "update_prefill": round(upd_ms, 4), "logprob": round(lp_ms, 4)},
         "prompt_prefill_tflops": round(pre_tflops, 2),
         "logprob_gbs": round(lp_gbs, 2),
         "logprob_frac_hbm": round(lp_gbs / HBM_PEAK_GBS, 4),
+        "kv_write_gbs": round(kvw_gbs, 2),
+        "kv_write_frac_hbm": round(kvw_gbs / HBM_PEAK_GBS, 4),
         "bitwise_match_pct": round(bitwise_pct, 4),
         "bitwise_rows": [n_match, n_rows],
         "logprob_batch_invariant": ratio_one,

@@ -161,6 +161,39 @@ uattn_status uattn_logprob(const void* logits, int64_t row_stride, const int32_t
                            int32_t num_rows, int32_t vocab, float inv_temperature, float* logp,
                            void* stream);
 
+/*
+ * Indexed write of new keys and values into the paged cache (the rollout-only
+ * KV-cache operator whose post-write state is checked exactly, Section 6 Q3
+ * and its table of prescribed bitwise checks):
+ *
+ *   for every token n with positions[n] >= 0, every kv head h, every d:
+ *     page = block_table[seq_idx[n] * max_pages_per_seq + positions[n] / page_size]
+ *     k_pages[page][h][positions[n] % page_size][:] = k_new[n * token_stride + h * head_dim + :]
+ *     v_pages[...same...]                             = v_new[n * token_stride + h * head_dim + :]
+ *
+ *   k_new, v_new   token rows of num_kv_heads * head_dim bf16 (heads contiguous),
+ *                  token_stride elements apart (>= num_kv_heads * head_dim, a
+ *                  multiple of 8); 16-byte aligned
+ *   block_table    [batch, max_pages_per_seq] int32 (the decode layout)
+ *   seq_idx        [num_tokens] int32, row of block_table of each token
+ *   positions      [num_tokens] int32, position of each token in its sequence
+ *                  (< 0: padding, the token is not written)
+ *   k_pages, v_pages  [num_pages, num_kv_heads, page_size, head_dim] bf16 (written
+ *                  in place; every slot no token maps to keeps its bits)
+ *
+ * A token whose seq_idx is outside [0, batch), whose position / page_size is
+ * not below max_pages_per_seq, or whose table entry is outside
+ * [0, num_pages) is not written (device values are trusted but never used to
+ * form an address outside the tensors).  Two tokens mapping to one slot
+ * write it in unspecified order.  head_dim 64 or 128; page_size a power of
+ * two >= 16.  Values are copied bit for bit.
+ */
+uattn_status uattn_kv_write(const void* k_new, const void* v_new, int64_t token_stride,
+                            const int32_t* block_table, const int32_t* seq_idx, const int32_t* positions,
+                            int32_t num_tokens, int32_t batch, int32_t max_pages_per_seq, int32_t page_size,
+                            int32_t num_pages, int32_t num_kv_heads, int32_t head_dim,
+                            void* k_pages, void* v_pages, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

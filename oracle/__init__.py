@@ -23,4 +23,5 @@ from .attention import (  # noqa: F401
     tile_emulate_fp32,
     to_bf16_bits,
 )
+from .kv_cache import kv_write  # noqa: F401
 from .logprob import logprob_fp64  # noqa: F401

@@ -206,4 +206,47 @@ uattn_status uattn_logprob(const void* logits, int64_t row_stride, const int32_t
   return uattn::launch_logprob(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
 }
 
+uattn_status uattn_kv_write(const void* k_new, const void* v_new, int64_t token_stride, const int32_t* block_table,
+                            const int32_t* seq_idx, const int32_t* positions, int32_t num_tokens, int32_t batch,
+                            int32_t max_pages_per_seq, int32_t page_size, int32_t num_pages, int32_t num_kv_heads,
+                            int32_t head_dim, void* k_pages, void* v_pages, void* stream) {
+  if (num_tokens < 0 || batch < 0 || max_pages_per_seq < 0 || num_pages < 0 || num_kv_heads <= 0) return UATTN_EINVAL;
+  if (head_dim != 64 && head_dim != 128) return UATTN_EUNSUPPORTED;
+  if (page_size < 16 || (page_size & (page_size - 1)) != 0) return UATTN_EUNSUPPORTED;
+  if (token_stride < static_cast<int64_t>(num_kv_heads) * head_dim || (token_stride % 8) != 0) return UATTN_EINVAL;
+  if (num_tokens == 0 || batch == 0 || max_pages_per_seq == 0 || num_pages == 0) return UATTN_OK;
+  if (!k_new || !v_new || !block_table || !seq_idx || !positions || !k_pages || !v_pages) return UATTN_EINVAL;
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pages) || !aligned16(v_pages)) return UATTN_EINVAL;
+  if (validate_env()) {
+    std::vector<int32_t> si, ps, bt;
+    if (!copy_back(si, seq_idx, static_cast<size_t>(num_tokens)) ||
+        !copy_back(ps, positions, static_cast<size_t>(num_tokens)) ||
+        !copy_back(bt, block_table, static_cast<size_t>(batch) * max_pages_per_seq))
+      return UATTN_EINVAL;
+    for (int32_t n = 0; n < num_tokens; ++n) {
+      if (ps[n] < 0) continue;
+      if (si[n] < 0 || si[n] >= batch || ps[n] / page_size >= max_pages_per_seq) return UATTN_EINVAL;
+      const int32_t pg = bt[static_cast<size_t>(si[n]) * max_pages_per_seq + ps[n] / page_size];
+      if (pg < 0 || pg >= num_pages) return UATTN_EINVAL;
+    }
+  }
+  uattn::KvWriteLaunch a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.token_stride = token_stride;
+  a.block_table = block_table;
+  a.seq_idx = seq_idx;
+  a.positions = positions;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.num_tokens = num_tokens;
+  a.batch = batch;
+  a.max_pages_per_seq = max_pages_per_seq;
+  a.page_size = page_size;
+  a.num_pages = num_pages;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  return uattn::launch_kv_write(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
+}
+
 }  // extern "C"

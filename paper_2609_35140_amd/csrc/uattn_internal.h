@@ -57,6 +57,20 @@ struct LogprobLaunch {
   float inv_temperature;
 };
 
+struct KvWriteLaunch {
+  const void* k_new;
+  const void* v_new;
+  int64_t token_stride;
+  const int32_t* block_table;
+  const int32_t* seq_idx;
+  const int32_t* positions;
+  void* k_pages;
+  void* v_pages;
+  int32_t num_tokens, batch, max_pages_per_seq, page_size, num_pages, num_kv_heads, head_dim;
+};
+
+hipError_t launch_kv_write(const KvWriteLaunch& a, hipStream_t stream);
+
 // Compute units of the current device (cached per device; 256 if the query fails).
 int32_t device_cus();
 

@@ -47,6 +47,9 @@ def _load():
                                  c_p, c_p, c_p, c_sz, c_p]
     lib.uattn_logprob.restype = c_i32
     lib.uattn_logprob.argtypes = [c_p, c_i64, c_p, c_i32, c_i32, c_f, c_p, c_p]
+    lib.uattn_kv_write.restype = c_i32
+    lib.uattn_kv_write.argtypes = [c_p, c_p, c_i64, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                   c_p, c_p, c_p]
     _lib = lib
     return lib
 
@@ -211,6 +214,35 @@ def logprob(logits, targets, inv_temperature: float = 1.0, out=None, stream=None
     _check(_load().uattn_logprob(_ptr(logits), logits.stride(0), _ptr(targets), T, V, float(inv_temperature),
                                  _ptr(out), _stream(stream)))
     return out
+
+
+def kv_write(k_new, v_new, block_table, seq_idx, positions, k_pages, v_pages, stream=None):
+    """Write new K/V token rows into the paged cache in place (uattn_kv_write).
+
+      k_new, v_new   [N, Hkv, d] bf16 (token rows may be strided: stride(0) elements apart)
+      block_table    [B, maxp] int32; seq_idx, positions [N] int32 (position < 0: padding)
+      k_pages, v_pages  [P, Hkv, page, d] bf16, updated in place
+    """
+    import torch
+    for name, t in (("k_pages", k_pages), ("v_pages", v_pages)):
+        _bf16_cuda(t, name)
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _need(t.is_cuda and t.dtype == torch.bfloat16, f"{name} must be a bfloat16 GPU tensor")
+    _need(k_new.dim() == 3 and v_new.shape == k_new.shape, "k_new/v_new must be [N,Hkv,d]")
+    N, hkv, d = k_new.shape
+    _need(k_new.stride(2) == 1 and k_new.stride(1) == d and v_new.stride() == k_new.stride(),
+          "k_new/v_new: heads and d must be contiguous, both with the same token stride")
+    P, hkv2, page, d2 = k_pages.shape
+    _need(hkv2 == hkv and d2 == d and v_pages.shape == k_pages.shape and k_pages.is_contiguous()
+          and v_pages.is_contiguous(), "page shapes")
+    for name, t in (("block_table", block_table), ("seq_idx", seq_idx), ("positions", positions)):
+        _need(t.dtype == torch.int32 and t.is_cuda and t.is_contiguous(), f"{name} must be int32 on the GPU")
+    _need(block_table.dim() == 2 and seq_idx.shape == (N,) and positions.shape == (N,), "index shapes")
+    B, maxp = block_table.shape
+    _check(_load().uattn_kv_write(_ptr(k_new), _ptr(v_new), k_new.stride(0), _ptr(block_table), _ptr(seq_idx),
+                                  _ptr(positions), N, B, maxp, page, P, hkv, d, _ptr(k_pages), _ptr(v_pages),
+                                  _stream(stream)))
+    return k_pages, v_pages
 
 
 def raw_call(name: str, *args) -> int:

@@ -27,7 +27,7 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ["uattn_prefill", "uattn_decode", "uattn_decode_workspace_bytes", "uattn_logprob",
+    for n in ["uattn_prefill", "uattn_decode", "uattn_decode_workspace_bytes", "uattn_logprob", "uattn_kv_write",
               "uattn_status_string", "uattn_abi_version"]:
         assert n in names
 
@@ -113,6 +113,23 @@ def test_decode_argument_checks(lib, kw, code):
 ])
 def test_logprob_argument_checks(lib, args, code):
     assert lib.uattn_logprob(*args) == code
+
+
+def _kv_write(lib, **kw):
+    a = dict(kn=P(16), vn=P(16), stride=256, bt=P(16), si=P(16), pos=P(16), N=4, B=2, maxp=4, page=16, npages=10,
+             hkv=2, d=128, kp=P(16), vp=P(16), stream=None)
+    a.update(kw)
+    return lib.uattn_kv_write(a["kn"], a["vn"], a["stride"], a["bt"], a["si"], a["pos"], a["N"], a["B"], a["maxp"],
+                              a["page"], a["npages"], a["hkv"], a["d"], a["kp"], a["vp"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=96), 2), (dict(page=24), 2), (dict(page=8), 2), (dict(stride=200), 1), (dict(stride=260), 1),
+    (dict(hkv=0), 1), (dict(N=-1), 1), (dict(kn=None), 1), (dict(vp=None), 1), (dict(pos=None), 1),
+    (dict(kn=P(18)), 1), (dict(kp=P(24)), 1), (dict(N=0), 0), (dict(npages=0), 0), (dict(B=0), 0),
+])
+def test_kv_write_argument_checks(lib, kw, code):
+    assert _kv_write(lib, **kw) == code
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
