@@ -9,7 +9,9 @@ heads, head_dim 128, bf16 ~ N(0, 0.25), paged KV with 64-token pages):
      and the indexed write of the prompts' K/V into the paged cache
   2. rollout decode of the 3072 response tokens,
      token by token, batch 8, against the paged cache (token-wise entry point)
-  3. policy-update prefill over the 8 full trajectories (full-sequence entry point)
+  3. Q/K RMSNorm + NeoX RoPE over the 8 full trajectories, then the policy-update
+     prefill over them (full-sequence entry point; it runs on the raw Q/K so
+     that the bitwise comparison with the decode rows uses the same inputs)
   4. log-probabilities of the 8 x 3072 response tokens over a 151,936-entry
      vocabulary (bf16 logits ~ N(0, 4))
 
@@ -146,6 +148,12 @@ def main():
     # the rollout writes the prompt's K/V into the paged cache (same bits the cache already holds)
     seq_p = torch.from_numpy(np.repeat(np.arange(B, dtype=np.int32), P)).to(dev)
     pos_p = torch.from_numpy(np.tile(np.arange(P, dtype=np.int32), B)).to(dev)
+    # Q/K RMSNorm + NeoX RoPE over the full trajectories (its own buffers; the attention inputs stay raw)
+    pos_full = torch.from_numpy(np.concatenate([np.arange(n, dtype=np.int32) for n in w.seq_lens])).to(dev)
+    qn_w = inputs.normal_bf16_device((d,), 1.0, 90, 0)
+    kn_w = inputs.normal_bf16_device((d,), 1.0, 90, 1)
+    cos_sin = uattn.rope_cache(L, d, 1e6)
+    q_rope, k_rope = torch.empty_like(q), torch.empty_like(k)
     # decode steps: query of token P+s of every sequence; context P+s+1
     tok = torch.from_numpy((cu[:B][None, :] + P + np.arange(R)[:, None]).astype(np.int64)).to(dev)  # [R, B]
     q_steps = q[tok.reshape(-1)].reshape(R, B, hq, d).contiguous()
@@ -199,6 +207,9 @@ def main():
             for s_ in range(R):
                 steps.run(s_)
         ev["dec"].b.record()
+        ev["nr"].a.record()
+        uattn.qk_norm_rope(q, k, pos_full, qn_w, kn_w, cos_sin, q_out=q_rope, k_out=k_rope)
+        ev["nr"].b.record()
         ev["upd"].a.record()
         uattn.prefill(q, k, v, cu_dev, L, out=out_full)
         ev["upd"].b.record()
@@ -207,7 +218,8 @@ def main():
         ev["lp"].b.record()
 
     def new_events():
-        return {"pre": Ev(torch), "kvw": Ev(torch), "upd": Ev(torch), "lp": Ev(torch), "dec": Ev(torch)}
+        return {"pre": Ev(torch), "kvw": Ev(torch), "nr": Ev(torch), "upd": Ev(torch), "lp": Ev(torch),
+                "dec": Ev(torch)}
 
     for i in range(args.warmup):
         step(new_events())
@@ -227,6 +239,7 @@ def main():
     upd_ms = sum(e["upd"].ms() for e in evs) / K
     lp_ms = sum(e["lp"].ms() for e in evs) / K
     kvw_ms = sum(e["kvw"].ms() for e in evs) / K
+    nr_ms = sum(e["nr"].ms() for e in evs) / K
     dec_wall_ms = sum(e["dec"].ms() for e in evs) / K
     dec_kernel_ms = dec_wall_ms
     step_ms = wall / K * 1e3
@@ -241,6 +254,8 @@ def main():
     lp_gbs = lp_bytes / (lp_ms * 1e-3) / 1e9
     kvw_bytes = float(B * P) * hkv * d * 2 * 2 * 2      # K and V rows read once and written once
     kvw_gbs = kvw_bytes / (kvw_ms * 1e-3) / 1e9
+    nr_bytes = float(q.numel() + k.numel()) * 2 * 2    # every q and k element read once and written once
+    nr_gbs = nr_bytes / (nr_ms * 1e-3) / 1e9
 
     # ------------------------------------------------------------------ bitwise Eq. (1)
     full_bits = out_full.view(torch.int16)
@@ -314,12 +329,15 @@ def main():
             "avg_launch_ms": round(upd_ms, 4),
         },
         "phases_ms": {"prompt_prefill": round(pre_ms, 4), "kv_write": round(kvw_ms, 4), "decode": round(dec_wall_ms, 3),
+                      "qk_norm_rope": round(nr_ms, 4),
                       "update_prefill": round(upd_ms, 4), "logprob": round(lp_ms, 4)},
         "prompt_prefill_tflops": round(pre_tflops, 2),
         "logprob_gbs": round(lp_gbs, 2),
         "logprob_frac_hbm": round(lp_gbs / HBM_PEAK_GBS, 4),
         "kv_write_gbs": round(kvw_gbs, 2),
         "kv_write_frac_hbm": round(kvw_gbs / HBM_PEAK_GBS, 4),
+        "qk_norm_rope_gbs": round(nr_gbs, 2),
+        "qk_norm_rope_frac_hbm": round(nr_gbs / HBM_PEAK_GBS, 4),
         "bitwise_match_pct": round(bitwise_pct, 4),
         "bitwise_rows": [n_match, n_rows],
         "logprob_batch_invariant": ratio_one,

@@ -194,6 +194,42 @@ uattn_status uattn_kv_write(const void* k_new, const void* v_new, int64_t token_
                             int32_t num_pages, int32_t num_kv_heads, int32_t head_dim,
                             void* k_pages, void* v_pages, void* stream);
 
+/*
+ * Query/key normalization and rotary position embedding before attention, in
+ * one pass (the Q RMSNorm, K RMSNorm and NeoX RoPE operators of Section 6 Q3,
+ * whose full-sequence and token-wise outputs must agree bit for bit).  For
+ * every token t and every head row x = q[t][h][:] (and k[t][h][:]):
+ *
+ *   r      = 1 / sqrt(sum_i x_i^2 / head_dim + eps)     (fp32, fixed order)
+ *   y_i    = bf16( w_i * bf16(x_i * r) )                 (w = q_weight or k_weight)
+ *   for i < head_dim / 2, with c = cos_sin[pos][i][0], s = cos_sin[pos][i][1], pos = positions[t]:
+ *     out_i              = bf16( y_i * c - y_{i+head_dim/2} * s )
+ *     out_{i+head_dim/2} = bf16( y_{i+head_dim/2} * c + y_i * s )
+ *
+ *   q, k           [num_tokens, num_q_heads | num_kv_heads, head_dim] bf16, contiguous
+ *   positions      [num_tokens] int32 in [0, max_position)
+ *   q_weight, k_weight  [head_dim] bf16
+ *   cos_sin        [max_position, head_dim / 2, 2] fp32 (uattn_rope_cache)
+ *   q_out, k_out   same shapes as q, k (written; may be q, k themselves)
+ *
+ * Every row is computed by the same instruction sequence whatever num_tokens
+ * or the row's place in the batch.  A token whose position is outside
+ * [0, max_position) gets NaN rows.  head_dim 64 or 128; every tensor
+ * argument except positions 16-byte aligned.
+ */
+uattn_status uattn_qk_norm_rope(const void* q, const void* k, const int32_t* positions, const void* q_weight,
+                                const void* k_weight, float eps, const float* cos_sin, int32_t max_position,
+                                int32_t num_tokens, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                void* q_out, void* k_out, void* stream);
+
+/*
+ * The rotary table for uattn_qk_norm_rope (NeoX layout):
+ *   cos_sin[p][i][0] = fp32(cos(p * theta^(-2i/head_dim))),  cos_sin[p][i][1] = fp32(sin(...))
+ * with the angle and both functions evaluated in fp64, for p < max_position
+ * and i < head_dim / 2.  theta > 1.
+ */
+uattn_status uattn_rope_cache(float* cos_sin, int32_t max_position, int32_t head_dim, double theta, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

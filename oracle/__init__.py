@@ -25,3 +25,4 @@ from .attention import (  # noqa: F401
 )
 from .kv_cache import kv_write  # noqa: F401
 from .logprob import logprob_fp64  # noqa: F401
+from .norm_rope import qk_norm_rope, rms_norm_bf16, rope_neox, rope_table  # noqa: F401

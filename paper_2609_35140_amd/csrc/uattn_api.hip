@@ -249,4 +249,45 @@ uattn_status uattn_kv_write(const void* k_new, const void* v_new, int64_t token_
   return uattn::launch_kv_write(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
 }
 
+uattn_status uattn_qk_norm_rope(const void* q, const void* k, const int32_t* positions, const void* q_weight,
+                                const void* k_weight, float eps, const float* cos_sin, int32_t max_position,
+                                int32_t num_tokens, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                void* q_out, void* k_out, void* stream) {
+  if (num_tokens < 0 || num_q_heads <= 0 || num_kv_heads <= 0 || max_position <= 0) return UATTN_EINVAL;
+  if (!(eps >= 0.f) || !(eps < __builtin_inff())) return UATTN_EINVAL;
+  if (head_dim != 64 && head_dim != 128) return UATTN_EUNSUPPORTED;
+  if (num_tokens == 0) return UATTN_OK;
+  if (!q || !k || !positions || !q_weight || !k_weight || !cos_sin || !q_out || !k_out) return UATTN_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(q_out) || !aligned16(k_out) || !aligned16(cos_sin) ||
+      !aligned16(q_weight) || !aligned16(k_weight))
+    return UATTN_EINVAL;
+  uattn::NormRopeLaunch a;
+  a.q = q;
+  a.k = k;
+  a.positions = positions;
+  a.q_weight = q_weight;
+  a.k_weight = k_weight;
+  a.cos_sin = cos_sin;
+  a.q_out = q_out;
+  a.k_out = k_out;
+  a.eps = eps;
+  a.max_position = max_position;
+  a.num_tokens = num_tokens;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  return uattn::launch_qk_norm_rope(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
+}
+
+uattn_status uattn_rope_cache(float* cos_sin, int32_t max_position, int32_t head_dim, double theta, void* stream) {
+  if (max_position < 0 || !(theta > 1.0) || !(theta < 1e300)) return UATTN_EINVAL;
+  if (head_dim != 64 && head_dim != 128) return UATTN_EUNSUPPORTED;
+  if (max_position == 0) return UATTN_OK;
+  if (!cos_sin || !aligned16(cos_sin)) return UATTN_EINVAL;
+  return uattn::launch_rope_cache(cos_sin, max_position, head_dim, theta, static_cast<hipStream_t>(stream)) ==
+                 hipSuccess
+             ? UATTN_OK
+             : UATTN_ELAUNCH;
+}
+
 }  // extern "C"

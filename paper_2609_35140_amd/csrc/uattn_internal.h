@@ -71,6 +71,22 @@ struct KvWriteLaunch {
 
 hipError_t launch_kv_write(const KvWriteLaunch& a, hipStream_t stream);
 
+struct NormRopeLaunch {
+  const void* q;
+  const void* k;
+  const int32_t* positions;
+  const void* q_weight;
+  const void* k_weight;
+  const float* cos_sin;
+  void* q_out;
+  void* k_out;
+  float eps;
+  int32_t max_position, num_tokens, num_q_heads, num_kv_heads, head_dim;
+};
+
+hipError_t launch_qk_norm_rope(const NormRopeLaunch& a, hipStream_t stream);
+hipError_t launch_rope_cache(float* cos_sin, int32_t max_position, int32_t head_dim, double theta, hipStream_t stream);
+
 // Compute units of the current device (cached per device; 256 if the query fails).
 int32_t device_cus();
 

@@ -47,6 +47,11 @@ def _load():
                                  c_p, c_p, c_p, c_sz, c_p]
     lib.uattn_logprob.restype = c_i32
     lib.uattn_logprob.argtypes = [c_p, c_i64, c_p, c_i32, c_i32, c_f, c_p, c_p]
+    lib.uattn_qk_norm_rope.restype = c_i32
+    lib.uattn_qk_norm_rope.argtypes = [c_p, c_p, c_p, c_p, c_p, c_f, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_p, c_p,
+                                       c_p]
+    lib.uattn_rope_cache.restype = c_i32
+    lib.uattn_rope_cache.argtypes = [c_p, c_i32, c_i32, ctypes.c_double, c_p]
     lib.uattn_kv_write.restype = c_i32
     lib.uattn_kv_write.argtypes = [c_p, c_p, c_i64, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
                                    c_p, c_p, c_p]
@@ -243,6 +248,46 @@ def kv_write(k_new, v_new, block_table, seq_idx, positions, k_pages, v_pages, st
                                   _ptr(positions), N, B, maxp, page, P, hkv, d, _ptr(k_pages), _ptr(v_pages),
                                   _stream(stream)))
     return k_pages, v_pages
+
+
+def rope_cache(max_position: int, head_dim: int, theta: float, out=None, stream=None):
+    """The NeoX rotary table [max_position, head_dim/2, 2] fp32 (uattn_rope_cache)."""
+    import torch
+    if out is None:
+        out = torch.empty((max_position, head_dim // 2, 2), dtype=torch.float32, device="cuda")
+    _need(out.dtype == torch.float32 and out.is_cuda and out.is_contiguous()
+          and tuple(out.shape) == (max_position, head_dim // 2, 2), "out must be [max_position, head_dim/2, 2] fp32")
+    _check(_load().uattn_rope_cache(_ptr(out), max_position, head_dim, float(theta), _stream(stream)))
+    return out
+
+
+def qk_norm_rope(q, k, positions, q_weight, k_weight, cos_sin, eps: float = 1e-6, q_out=None, k_out=None,
+                 stream=None):
+    """RMSNorm of every q and k head row, then NeoX rotary embedding (uattn_qk_norm_rope).
+
+      q [T, Hq, d], k [T, Hkv, d] bf16; positions [T] int32; q_weight, k_weight [d] bf16;
+      cos_sin [max_position, d/2, 2] fp32.  Outputs may be q and k themselves (in place).
+    """
+    import torch
+    for name, t in (("q", q), ("k", k), ("q_weight", q_weight), ("k_weight", k_weight)):
+        _bf16_cuda(t, name)
+    _need(q.dim() == 3 and k.dim() == 3 and q.shape[0] == k.shape[0] and q.shape[2] == k.shape[2], "q/k shapes")
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    _need(q_weight.shape == (d,) and k_weight.shape == (d,), "weights must be [d]")
+    _need(positions.dtype == torch.int32 and positions.is_cuda and positions.shape == (T,) and positions.is_contiguous(),
+          "positions must be [T] int32 on the GPU")
+    _need(cos_sin.dtype == torch.float32 and cos_sin.is_cuda and cos_sin.is_contiguous() and cos_sin.dim() == 3
+          and cos_sin.shape[1:] == (d // 2, 2), "cos_sin must be [max_position, d/2, 2] fp32")
+    if q_out is None:
+        q_out = torch.empty_like(q)
+    if k_out is None:
+        k_out = torch.empty_like(k)
+    _need(q_out.shape == q.shape and k_out.shape == k.shape, "output shapes")
+    _check(_load().uattn_qk_norm_rope(_ptr(q), _ptr(k), _ptr(positions), _ptr(q_weight), _ptr(k_weight), float(eps),
+                                      _ptr(cos_sin), cos_sin.shape[0], T, hq, hkv, d, _ptr(q_out), _ptr(k_out),
+                                      _stream(stream)))
+    return q_out, k_out
 
 
 def raw_call(name: str, *args) -> int:

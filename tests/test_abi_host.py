@@ -138,3 +138,23 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(uattn, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(uattn.UattnError):
         uattn.abi_version()
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=96), 2), (dict(eps=-1.0), 1), (dict(eps=float("nan")), 1), (dict(maxpos=0), 1), (dict(hq=0), 1),
+    (dict(q=None), 1), (dict(cs=None), 1), (dict(cs=P(20)), 1), (dict(T=-1), 1), (dict(T=0), 0),
+])
+def test_qk_norm_rope_argument_checks(lib, kw, code):
+    a = dict(q=P(16), k=P(16), pos=P(16), qw=P(16), kw=P(16), eps=1e-6, cs=P(16), maxpos=10, T=4, hq=4, hkv=2, d=128,
+             qo=P(16), ko=P(16), stream=None)
+    a.update(kw)
+    assert lib.uattn_qk_norm_rope(a["q"], a["k"], a["pos"], a["qw"], a["kw"], a["eps"], a["cs"], a["maxpos"], a["T"],
+                                  a["hq"], a["hkv"], a["d"], a["qo"], a["ko"], a["stream"]) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((P(16), 10, 96, 1e4, None), 2), ((P(16), 10, 128, 1.0, None), 1), ((P(16), -1, 128, 1e4, None), 1),
+    ((None, 10, 128, 1e4, None), 1), ((P(16), 0, 128, 1e4, None), 0),
+])
+def test_rope_cache_argument_checks(lib, args, code):
+    assert lib.uattn_rope_cache(*args) == code
