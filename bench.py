@@ -12,8 +12,8 @@ heads, head_dim 128, bf16 ~ N(0, 0.25), paged KV with 64-token pages):
   3. Q/K RMSNorm + NeoX RoPE over the 8 full trajectories, then the policy-update
      prefill over them (full-sequence entry point; it runs on the raw Q/K so
      that the bitwise comparison with the decode rows uses the same inputs)
-  4. log-probabilities of the 8 x 3072 response tokens over a 151,936-entry
-     vocabulary (bf16 logits ~ N(0, 4))
+  4. the batch-invariant LM head (hidden 4096 -> 151,936 logits, ~ N(0, 4)) of
+     the 8 x 3072 response tokens, and their log-probabilities
 
 Inputs are resident in HBM before the timed region.  Every phase is bracketed
 by HIP events on the stream it runs on; the 3072 decode launches are replayed
@@ -164,7 +164,12 @@ def main():
     out_full = torch.empty_like(q)
     # log-prob leg: one row per response token
     rows = B * R
-    logits = inputs.normal_bf16_device((rows, V), w.logit_sigma, 7, 0)
+    # LM head: hidden states [rows, Hq*d] ~ N(0,1) and weights ~ N(0, sigma^2/H), so the
+    # logits it produces are ~ N(0, logit_sigma^2); the log-prob leg reads them
+    H = hq * d
+    hidden = inputs.normal_bf16_device((rows, H), 1.0, 7, 1)
+    lm_w = inputs.normal_bf16_device((V, H), w.logit_sigma / float(np.sqrt(H)), 7, 2)
+    logits = torch.empty((rows, V), dtype=torch.bfloat16, device=dev)
     targets = torch.from_numpy(inputs.targets(rows, V)).to(dev)
     logp = torch.empty(rows, dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
@@ -213,13 +218,16 @@ def main():
         ev["upd"].a.record()
         uattn.prefill(q, k, v, cu_dev, L, out=out_full)
         ev["upd"].b.record()
+        ev["lm"].a.record()
+        uattn.lm_head(hidden, lm_w, out=logits)
+        ev["lm"].b.record()
         ev["lp"].a.record()
         uattn.logprob(logits, targets, out=logp)
         ev["lp"].b.record()
 
     def new_events():
-        return {"pre": Ev(torch), "kvw": Ev(torch), "nr": Ev(torch), "upd": Ev(torch), "lp": Ev(torch),
-                "dec": Ev(torch)}
+        return {"pre": Ev(torch), "kvw": Ev(torch), "nr": Ev(torch), "upd": Ev(torch), "lm": Ev(torch),
+                "lp": Ev(torch), "dec": Ev(torch)}
 
     for i in range(args.warmup):
         step(new_events())
@@ -240,6 +248,7 @@ def main():
     lp_ms = sum(e["lp"].ms() for e in evs) / K
     kvw_ms = sum(e["kvw"].ms() for e in evs) / K
     nr_ms = sum(e["nr"].ms() for e in evs) / K
+    lm_ms = sum(e["lm"].ms() for e in evs) / K
     dec_wall_ms = sum(e["dec"].ms() for e in evs) / K
     dec_kernel_ms = dec_wall_ms
     step_ms = wall / K * 1e3
@@ -256,6 +265,8 @@ def main():
     kvw_gbs = kvw_bytes / (kvw_ms * 1e-3) / 1e9
     nr_bytes = float(q.numel() + k.numel()) * 2 * 2    # every q and k element read once and written once
     nr_gbs = nr_bytes / (nr_ms * 1e-3) / 1e9
+    lm_flop = 2.0 * rows * V * H
+    lm_tflops = lm_flop / (lm_ms * 1e-3) / 1e12
 
     # ------------------------------------------------------------------ bitwise Eq. (1)
     full_bits = out_full.view(torch.int16)
@@ -329,7 +340,7 @@ def main():
             "avg_launch_ms": round(upd_ms, 4),
         },
         "phases_ms": {"prompt_prefill": round(pre_ms, 4), "kv_write": round(kvw_ms, 4), "decode": round(dec_wall_ms, 3),
-                      "qk_norm_rope": round(nr_ms, 4),
+                      "qk_norm_rope": round(nr_ms, 4), "lm_head": round(lm_ms, 4),
                       "update_prefill": round(upd_ms, 4), "logprob": round(lp_ms, 4)},
         "prompt_prefill_tflops": round(pre_tflops, 2),
         "logprob_gbs": round(lp_gbs, 2),
@@ -338,6 +349,8 @@ def main():
         "kv_write_frac_hbm": round(kvw_gbs / HBM_PEAK_GBS, 4),
         "qk_norm_rope_gbs": round(nr_gbs, 2),
         "qk_norm_rope_frac_hbm": round(nr_gbs / HBM_PEAK_GBS, 4),
+        "lm_head_tflops": round(lm_tflops, 2),
+        "lm_head_frac_mfma": round(lm_tflops / BF16_PEAK_TFLOPS, 4),
         "bitwise_match_pct": round(bitwise_pct, 4),
         "bitwise_rows": [n_match, n_rows],
         "logprob_batch_invariant": ratio_one,

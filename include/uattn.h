@@ -230,6 +230,28 @@ uattn_status uattn_qk_norm_rope(const void* q, const void* k, const int32_t* pos
  */
 uattn_status uattn_rope_cache(float* cos_sin, int32_t max_position, int32_t head_dim, double theta, void* stream);
 
+/*
+ * Batch-invariant LM head: the logits the log-probability reads (Section 3.1
+ * requires the same deterministic logit processing in both regimes, so the
+ * logits themselves must not depend on how many rows are computed together):
+ *
+ *   logits[t][v] = bf16( sum_k hidden[t][k] * weight[v][k] )
+ *
+ * accumulated in fp32 on v_mfma_f32_16x16x32_bf16 over k in ascending 32-wide
+ * steps from zero; no split over k, and the tiling over t never changes a
+ * row's arithmetic, so a row's logits are bit-identical whatever num_rows or
+ * the row's place in the batch.
+ *
+ *   hidden   [num_rows, hidden_stride] bf16, first hidden_dim used
+ *   weight   [vocab, weight_stride] bf16, first hidden_dim used
+ *   logits   [num_rows, logits_stride] bf16, first vocab written
+ *   hidden_dim a multiple of 64; strides >= the used widths and multiples of
+ *   8 elements; pointers 16-byte aligned.
+ */
+uattn_status uattn_lm_head(const void* hidden, int64_t hidden_stride, const void* weight, int64_t weight_stride,
+                           int32_t num_rows, int32_t vocab, int32_t hidden_dim, void* logits, int64_t logits_stride,
+                           void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -290,4 +290,26 @@ uattn_status uattn_rope_cache(float* cos_sin, int32_t max_position, int32_t head
              : UATTN_ELAUNCH;
 }
 
+uattn_status uattn_lm_head(const void* hidden, int64_t hidden_stride, const void* weight, int64_t weight_stride,
+                           int32_t num_rows, int32_t vocab, int32_t hidden_dim, void* logits, int64_t logits_stride,
+                           void* stream) {
+  if (num_rows < 0 || vocab < 0 || hidden_dim <= 0 || (hidden_dim % 64) != 0) return UATTN_EINVAL;
+  if (hidden_stride < hidden_dim || weight_stride < hidden_dim || logits_stride < vocab) return UATTN_EINVAL;
+  if ((hidden_stride % 8) != 0 || (weight_stride % 8) != 0 || (logits_stride % 8) != 0) return UATTN_EINVAL;
+  if (num_rows == 0 || vocab == 0) return UATTN_OK;
+  if (!hidden || !weight || !logits) return UATTN_EINVAL;
+  if (!aligned16(hidden) || !aligned16(weight) || !aligned16(logits)) return UATTN_EINVAL;
+  uattn::LmHeadLaunch a;
+  a.hidden = hidden;
+  a.hidden_stride = hidden_stride;
+  a.weight = weight;
+  a.weight_stride = weight_stride;
+  a.logits = logits;
+  a.logits_stride = logits_stride;
+  a.num_rows = num_rows;
+  a.vocab = vocab;
+  a.hidden_dim = hidden_dim;
+  return uattn::launch_lm_head(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
+}
+
 }  // extern "C"

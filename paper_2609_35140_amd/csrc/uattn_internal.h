@@ -87,6 +87,18 @@ struct NormRopeLaunch {
 hipError_t launch_qk_norm_rope(const NormRopeLaunch& a, hipStream_t stream);
 hipError_t launch_rope_cache(float* cos_sin, int32_t max_position, int32_t head_dim, double theta, hipStream_t stream);
 
+struct LmHeadLaunch {
+  const void* hidden;
+  int64_t hidden_stride;
+  const void* weight;
+  int64_t weight_stride;
+  void* logits;
+  int64_t logits_stride;
+  int32_t num_rows, vocab, hidden_dim;
+};
+
+hipError_t launch_lm_head(const LmHeadLaunch& a, hipStream_t stream);
+
 // Compute units of the current device (cached per device; 256 if the query fails).
 int32_t device_cus();
 

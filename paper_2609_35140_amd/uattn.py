@@ -52,6 +52,8 @@ def _load():
                                        c_p]
     lib.uattn_rope_cache.restype = c_i32
     lib.uattn_rope_cache.argtypes = [c_p, c_i32, c_i32, ctypes.c_double, c_p]
+    lib.uattn_lm_head.restype = c_i32
+    lib.uattn_lm_head.argtypes = [c_p, c_i64, c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_i64, c_p]
     lib.uattn_kv_write.restype = c_i32
     lib.uattn_kv_write.argtypes = [c_p, c_p, c_i64, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
                                    c_p, c_p, c_p]
@@ -288,6 +290,27 @@ def qk_norm_rope(q, k, positions, q_weight, k_weight, cos_sin, eps: float = 1e-6
                                       _ptr(cos_sin), cos_sin.shape[0], T, hq, hkv, d, _ptr(q_out), _ptr(k_out),
                                       _stream(stream)))
     return q_out, k_out
+
+
+def lm_head(hidden, weight, out=None, stream=None):
+    """Batch-invariant logits = bf16(hidden . weight^T) (uattn_lm_head).
+
+      hidden [T, H] bf16, weight [V, H] bf16 (rows may be strided); out [T, V] bf16 (row stride a multiple of 8).
+    """
+    import torch
+    for name, t in (("hidden", hidden), ("weight", weight)):
+        _need(t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 2 and t.stride(1) == 1,
+              f"{name} must be a 2-D bfloat16 GPU tensor with contiguous rows")
+    T, H = hidden.shape
+    V, H2 = weight.shape
+    _need(H2 == H, "hidden and weight widths differ")
+    if out is None:
+        stride = (V + 7) // 8 * 8
+        out = torch.empty((T, stride), dtype=torch.bfloat16, device=hidden.device)[:, :V]
+    _need(out.dtype == torch.bfloat16 and out.is_cuda and out.shape == (T, V) and out.stride(1) == 1, "out shape")
+    _check(_load().uattn_lm_head(_ptr(hidden), hidden.stride(0), _ptr(weight), weight.stride(0), T, V, H, _ptr(out),
+                                 out.stride(0), _stream(stream)))
+    return out
 
 
 def raw_call(name: str, *args) -> int:

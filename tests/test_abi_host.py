@@ -158,3 +158,13 @@ def test_qk_norm_rope_argument_checks(lib, kw, code):
 ])
 def test_rope_cache_argument_checks(lib, args, code):
     assert lib.uattn_rope_cache(*args) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(H=100), 1), (dict(H=0), 1), (dict(hs=512), 1), (dict(ws=1020), 1), (dict(os=1004), 1), (dict(os=999), 1),
+    (dict(h=P(18)), 1), (dict(o=None), 1), (dict(T=-1), 1), (dict(T=0), 0), (dict(V=0), 0),
+])
+def test_lm_head_argument_checks(lib, kw, code):
+    a = dict(h=P(16), hs=1024, w=P(16), ws=1024, T=4, V=1000, H=1024, o=P(16), os=1000, stream=None)
+    a.update(kw)
+    assert lib.uattn_lm_head(a["h"], a["hs"], a["w"], a["ws"], a["T"], a["V"], a["H"], a["o"], a["os"], a["stream"]) == code
