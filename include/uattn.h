@@ -252,6 +252,49 @@ uattn_status uattn_lm_head(const void* hidden, int64_t hidden_stride, const void
                            int32_t num_rows, int32_t vocab, int32_t hidden_dim, void* logits, int64_t logits_stride,
                            void* stream);
 
+/*
+ * Bytes of device workspace uattn_prefill_backward needs: two fp32 values
+ * per (token, q head).  Pure host arithmetic; 0 for invalid sizes.
+ */
+size_t uattn_prefill_backward_workspace_bytes(int32_t total_tokens, int32_t num_q_heads);
+
+/*
+ * Gradients of the full-sequence attention (the backward of uattn_prefill,
+ * which the policy update runs after its forward over every trajectory,
+ * Section 6 Q2).  The gradient of the Section 3.2 attention by the chain
+ * rule: for each (sequence, q head), with P the causal softmax weights,
+ *
+ *   dV = P^T dO,  dS = P * (dO V^T - D) with D_i = dO_i . O_i,
+ *   dQ = scale * dS K,  dK = scale * dS^T Q,
+ *
+ * dK and dV summed over the q heads of each group.  P is recomputed from the
+ * forward's log-sum-exp, D from its output.
+ *
+ *   q, k, v, cu_seqlens, num_seqs .. softmax_scale   exactly as passed to
+ *              uattn_prefill (same layouts, same clamping of cu_seqlens)
+ *   out        [total_tokens, num_q_heads, head_dim] bf16, uattn_prefill's output
+ *   dout       [total_tokens, num_q_heads, head_dim] bf16, upstream gradient
+ *   lse        [total_tokens, num_q_heads] fp32, uattn_prefill's log-sum-exp
+ *   dq         [total_tokens, num_q_heads, head_dim] bf16 (written)
+ *   dk, dv     [total_tokens, num_kv_heads, head_dim] bf16 (written; every row
+ *              of every sequence, zero-length sequences aside)
+ *   workspace  device scratch of at least
+ *              uattn_prefill_backward_workspace_bytes(total_tokens, num_q_heads)
+ *              bytes, 16-byte aligned; overwritten, no initial contents needed.
+ *              Calls that share a workspace must be ordered on one stream.
+ *
+ * Deterministic and batch-invariant: no atomics; each output row is summed by
+ * one workgroup in an order fixed by its own sequence (fp32 accumulation,
+ * bf16 P and dS as matrix operands, one bf16 rounding of each result), so
+ * repeated calls, and the same sequence in any batch, give identical bits.
+ * head_dim 64 or 128; bf16 tensors 16-byte aligned, lse 4-byte aligned.
+ */
+uattn_status uattn_prefill_backward(const void* q, const void* k, const void* v, const void* out, const void* dout,
+                                    const float* lse, const int32_t* cu_seqlens, int32_t num_seqs,
+                                    int32_t total_tokens, int32_t max_seqlen, int32_t num_q_heads,
+                                    int32_t num_kv_heads, int32_t head_dim, float softmax_scale, void* dq, void* dk,
+                                    void* dv, void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

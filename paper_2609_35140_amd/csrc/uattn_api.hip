@@ -312,4 +312,58 @@ uattn_status uattn_lm_head(const void* hidden, int64_t hidden_stride, const void
   return uattn::launch_lm_head(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
 }
 
+size_t uattn_prefill_backward_workspace_bytes(int32_t total_tokens, int32_t num_q_heads) {
+  if (total_tokens <= 0 || num_q_heads <= 0) return 0;
+  return uattn::backward_ws_bytes(total_tokens, num_q_heads);
+}
+
+uattn_status uattn_prefill_backward(const void* q, const void* k, const void* v, const void* out, const void* dout,
+                                    const float* lse, const int32_t* cu_seqlens, int32_t num_seqs,
+                                    int32_t total_tokens, int32_t max_seqlen, int32_t num_q_heads,
+                                    int32_t num_kv_heads, int32_t head_dim, float softmax_scale, void* dq, void* dk,
+                                    void* dv, void* workspace, size_t workspace_bytes, void* stream) {
+  if (num_seqs < 0 || total_tokens < 0 || max_seqlen < 0 || num_q_heads <= 0 || num_kv_heads <= 0)
+    return UATTN_EINVAL;
+  if (num_q_heads % num_kv_heads != 0 || !scale_ok(softmax_scale)) return UATTN_EINVAL;
+  if (head_dim != 64 && head_dim != 128) return UATTN_EUNSUPPORTED;
+  if (num_seqs > 65535) return UATTN_EUNSUPPORTED;
+  if (num_seqs == 0 || total_tokens == 0 || max_seqlen == 0) return UATTN_OK;
+  if (!q || !k || !v || !out || !dout || !lse || !cu_seqlens || !dq || !dk || !dv) return UATTN_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(dout) || !aligned16(dq) ||
+      !aligned16(dk) || !aligned16(dv) || (reinterpret_cast<uintptr_t>(lse) & 3u) != 0)
+    return UATTN_EINVAL;
+  const size_t need = uattn_prefill_backward_workspace_bytes(total_tokens, num_q_heads);
+  if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace)) return UATTN_EWORKSPACE;
+  if (validate_env()) {
+    std::vector<int32_t> cu;
+    if (!copy_back(cu, cu_seqlens, static_cast<size_t>(num_seqs) + 1)) return UATTN_EINVAL;
+    if (cu[0] != 0 || cu[num_seqs] != total_tokens) return UATTN_EINVAL;
+    for (int32_t s = 0; s < num_seqs; ++s) {
+      const int32_t len = cu[s + 1] - cu[s];
+      if (len < 0 || len > max_seqlen) return UATTN_EINVAL;
+    }
+  }
+  uattn::BackwardLaunch a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.dout = dout;
+  a.lse = lse;
+  a.cu_seqlens = cu_seqlens;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.workspace = workspace;
+  a.num_seqs = num_seqs;
+  a.total_tokens = total_tokens;
+  a.max_seqlen = max_seqlen;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.c = exp2_scale(softmax_scale);
+  a.scale = softmax_scale;
+  return uattn::launch_backward(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
+}
+
 }  // extern "C"

@@ -99,6 +99,26 @@ struct LmHeadLaunch {
 
 hipError_t launch_lm_head(const LmHeadLaunch& a, hipStream_t stream);
 
+struct BackwardLaunch {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* out;
+  const void* dout;
+  const float* lse;
+  const int32_t* cu_seqlens;
+  void* dq;
+  void* dk;
+  void* dv;
+  void* workspace;  // backward_ws_bytes(total_tokens, num_q_heads)
+  int32_t num_seqs, total_tokens, max_seqlen, num_q_heads, num_kv_heads, head_dim;
+  float c;      // fp32(scale * log2(e))
+  float scale;  // softmax scale
+};
+
+hipError_t launch_backward(const BackwardLaunch& a, hipStream_t stream);
+size_t backward_ws_bytes(int64_t total_tokens, int64_t num_q_heads);
+
 // Compute units of the current device (cached per device; 256 if the query fails).
 int32_t device_cus();
 

@@ -54,6 +54,11 @@ def _load():
     lib.uattn_rope_cache.argtypes = [c_p, c_i32, c_i32, ctypes.c_double, c_p]
     lib.uattn_lm_head.restype = c_i32
     lib.uattn_lm_head.argtypes = [c_p, c_i64, c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_i64, c_p]
+    lib.uattn_prefill_backward_workspace_bytes.restype = c_sz
+    lib.uattn_prefill_backward_workspace_bytes.argtypes = [c_i32, c_i32]
+    lib.uattn_prefill_backward.restype = c_i32
+    lib.uattn_prefill_backward.argtypes = [c_p, c_p, c_p, c_p, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                           c_i32, c_f, c_p, c_p, c_p, c_p, c_sz, c_p]
     lib.uattn_kv_write.restype = c_i32
     lib.uattn_kv_write.argtypes = [c_p, c_p, c_i64, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
                                    c_p, c_p, c_p]
@@ -136,6 +141,51 @@ def prefill(q, k, v, cu_seqlens, max_seqlen: int, softmax_scale: Optional[float]
                                  int(max_seqlen), hq, k.shape[1], d, float(softmax_scale), _ptr(out), _ptr(lse),
                                  _stream(stream)))
     return (out, lse) if lse is not None else out
+
+
+def prefill_backward_workspace_bytes(total_tokens: int, num_q_heads: int) -> int:
+    return int(_load().uattn_prefill_backward_workspace_bytes(int(total_tokens), int(num_q_heads)))
+
+
+def prefill_backward(q, k, v, out, dout, lse, cu_seqlens, max_seqlen: int, softmax_scale: Optional[float] = None,
+                     dq=None, dk=None, dv=None, workspace=None, stream=None):
+    """Gradients of the full-sequence attention (uattn_prefill_backward).
+
+    q, k, v, cu_seqlens, max_seqlen, softmax_scale as for prefill; out and lse
+    are prefill's outputs for them; dout [T,Hq,d] bf16 is the upstream
+    gradient.  Returns (dq [T,Hq,d], dk [T,Hkv,d], dv [T,Hkv,d]) bf16.
+    """
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v), ("out", out), ("dout", dout)):
+        _bf16_cuda(t, name)
+    _need(q.dim() == 3 and k.dim() == 3 and v.dim() == 3, "q/k/v must be [T, H, d]")
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    _need(k.shape == v.shape and k.shape[0] == T and k.shape[2] == d, "k/v shape mismatch")
+    _need(out.shape == q.shape and dout.shape == q.shape, "out/dout must match q")
+    _need(lse.dtype == torch.float32 and lse.is_cuda and lse.is_contiguous() and tuple(lse.shape) == (T, hq),
+          "lse must be [T,Hq] fp32 on the GPU")
+    _need(cu_seqlens.dtype == torch.int32 and cu_seqlens.is_cuda and cu_seqlens.is_contiguous(),
+          "cu_seqlens must be contiguous int32 on the GPU")
+    if softmax_scale is None:
+        softmax_scale = default_scale(d)
+    outs = []
+    for name, t, like in (("dq", dq, q), ("dk", dk, k), ("dv", dv, v)):
+        if t is None:
+            t = torch.empty_like(like)
+        else:
+            _bf16_cuda(t, name)
+            _need(t.shape == like.shape, f"{name} shape")
+        outs.append(t)
+    need = prefill_backward_workspace_bytes(T, hq)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)  # no initial contents needed
+    _check(_load().uattn_prefill_backward(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(cu_seqlens), cu_seqlens.numel() - 1, T,
+        int(max_seqlen), hq, hkv, d, float(softmax_scale), _ptr(outs[0]), _ptr(outs[1]), _ptr(outs[2]),
+        _ptr(workspace), workspace.numel() * workspace.element_size() if workspace is not None else 0,
+        _stream(stream)))
+    return tuple(outs)
 
 
 def decode_workspace_bytes(batch: int, max_seqlen: int, num_q_heads: int, head_dim: int) -> int:

@@ -168,3 +168,26 @@ def test_lm_head_argument_checks(lib, kw, code):
     a = dict(h=P(16), hs=1024, w=P(16), ws=1024, T=4, V=1000, H=1024, o=P(16), os=1000, stream=None)
     a.update(kw)
     assert lib.uattn_lm_head(a["h"], a["hs"], a["w"], a["ws"], a["T"], a["V"], a["H"], a["o"], a["os"], a["stream"]) == code
+
+
+def test_backward_workspace_bytes(lib):
+    from paper_2609_35140_amd import uattn
+    assert uattn.prefill_backward_workspace_bytes(1000, 32) == 2 * 1000 * 32 * 4   # D and lse*log2(e) per row
+    assert uattn.prefill_backward_workspace_bytes(0, 32) == 0
+    assert uattn.prefill_backward_workspace_bytes(5, -1) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(hq=3, hkv=2), 1), (dict(hkv=0), 1), (dict(ns=-1), 1), (dict(scale=0.0), 1), (dict(scale=float("nan")), 1),
+    (dict(d=96), 2), (dict(q=None), 1), (dict(out=None), 1), (dict(dout=None), 1), (dict(lse=None), 1),
+    (dict(dq=None), 1), (dict(dk=None), 1), (dict(dv=None), 1), (dict(dout=P(40)), 1), (dict(lse=P(18)), 1),
+    (dict(ws=None), 3), (dict(wsb=127), 3), (dict(ws=P(1032)), 3),
+    (dict(ns=0), 0), (dict(T=0), 0), (dict(maxs=0), 0),
+])
+def test_backward_argument_checks(lib, kw, code):
+    a = dict(q=P(16), k=P(16), v=P(16), out=P(16), dout=P(16), lse=P(16), cu=P(16), ns=1, T=4, maxs=4, hq=4, hkv=2,
+             d=128, scale=0.1, dq=P(16), dk=P(16), dv=P(16), ws=P(1024), wsb=128, stream=None)
+    a.update(kw)
+    assert lib.uattn_prefill_backward(a["q"], a["k"], a["v"], a["out"], a["dout"], a["lse"], a["cu"], a["ns"], a["T"],
+                                      a["maxs"], a["hq"], a["hkv"], a["d"], a["scale"], a["dq"], a["dk"], a["dv"],
+                                      a["ws"], a["wsb"], a["stream"]) == code

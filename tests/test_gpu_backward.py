@@ -1,0 +1,132 @@
+"""GPU attention backward: parity of dQ, dK, dV with the fp64 oracle, and the
+determinism the policy update needs (the same bits on every call and for a
+sequence in any batch).
+
+Inputs to the backward are what the training step feeds it: the GPU forward's
+own bf16 output and fp32 log-sum-exp.  The bound is derived from the
+kernels' arithmetic (fp32 scores and exp2, bf16 P and dS as matrix operands,
+fp32 accumulation, one bf16 rounding per result) plus the forward's bf16
+output entering D_i = dO_i . O_i; per element
+
+    |got - ref| <= 2^-7 * scale_elem + 2^-8 * |ref|
+
+with scale_elem from oracle.backward_error_scales (sum of |terms| of each
+gradient, with D's term size a_i).  The relative error of P from the saved
+log-sum-exp (whose normalizer sums bf16 weights) and its bf16 rounding are
+each at most 2^-9; the 2^-7 coefficient leaves a factor two over their sum.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_35140_amd import inputs
+
+pytestmark = pytest.mark.gpu
+gu = pytest.importorskip("gpu_util")
+
+A_COEF = 2.0 ** -7
+R_COEF = 2.0 ** -8
+
+
+@pytest.fixture(scope="module")
+def ua():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_35140_amd import uattn
+    uattn.lib()
+    return uattn
+
+
+def _inputs(lens, hq, hkv, d, sigma, tag):
+    cu = inputs.cu_seqlens(lens)
+    T = int(cu[-1])
+    key = (tag, hq, hkv, d, len(lens))
+    q = inputs.normal_bf16((T, hq, d), sigma, 81, *key, 0)
+    k = inputs.normal_bf16((T, hkv, d), sigma, 81, *key, 1)
+    v = inputs.normal_bf16((T, hkv, d), sigma, 81, *key, 2)
+    do = inputs.normal_bf16((T, hq, d), 1.0, 81, *key, 3)
+    return q, k, v, do, cu
+
+
+def _run(ua, q, k, v, do, cu, max_seqlen=None):
+    qd, kd, vd, dod = gu.dev(q), gu.dev(k), gu.dev(v), gu.dev(do)
+    cud = gu.dev_i32(cu)
+    ms = int(np.max(np.diff(cu))) if max_seqlen is None else max_seqlen
+    out, lse = ua.prefill(qd, kd, vd, cud, ms, return_lse=True)
+    return ua.prefill_backward(qd, kd, vd, out, dod, lse, cud, ms)
+
+
+def _check(name, got_bits, ref, scale):
+    got = oracle.bf16_to_f64(got_bits)
+    err = np.abs(got - ref)
+    bound = A_COEF * scale + R_COEF * np.abs(ref)
+    ratio = float(np.max(err / np.maximum(bound, 1e-300)))
+    print(f"  {name}: max err {err.max():.3e}  mean err {err.mean():.2e}  max err/bound {ratio:.3f}", flush=True)
+    assert np.all(np.isfinite(got)), name
+    assert np.all(err <= bound), (name, ratio)
+
+
+CASES = [  # (sequence lengths, Hq, Hkv, d, sigma)
+    ([300, 1, 129, 64, 0, 513], 8, 2, 128, 1.0),
+    ([77, 200], 4, 4, 64, 1.0),
+    ([257, 31, 1, 1], 16, 2, 64, 1.0),
+    ([1000, 390], 32, 8, 128, 0.25),
+    ([1], 4, 1, 128, 1.0),
+]
+
+
+@pytest.mark.parametrize("lens,hq,hkv,d,sigma", CASES)
+def test_matches_oracle(ua, lens, hq, hkv, d, sigma):
+    q, k, v, do, cu = _inputs(lens, hq, hkv, d, sigma, 0)
+    print(f"lens={lens} hq={hq} hkv={hkv} d={d} sigma={sigma}", flush=True)
+    dq, dk, dv = _run(ua, q, k, v, do, cu)
+    ref = oracle.attention_backward_fp64(q, k, v, do, cu)
+    sc = oracle.backward_error_scales(q, k, v, do, cu)
+    for name, got, r, s in zip(("dq", "dk", "dv"), (dq, dk, dv), ref, sc):
+        _check(name, gu.host_bits(got), r, s)
+
+
+def test_repeated_calls_are_bitwise_equal(ua):
+    q, k, v, do, cu = _inputs([700, 333, 64], 8, 2, 128, 1.0, 1)
+    first = [gu.host_bits(x) for x in _run(ua, q, k, v, do, cu)]
+    for _ in range(2):
+        again = [gu.host_bits(x) for x in _run(ua, q, k, v, do, cu)]
+        for a, b in zip(first, again):
+            assert np.array_equal(a, b)
+
+
+def test_batch_invariance(ua):
+    """A sequence's gradients do not depend on the other sequences, their
+    order, its place in the pack or max_seqlen."""
+    hq, hkv, d = 8, 2, 128
+    q, k, v, do, cu = _inputs([130, 517, 64, 1, 300], hq, hkv, d, 1.0, 2)
+    batch = [gu.host_bits(x) for x in _run(ua, q, k, v, do, cu, max_seqlen=1024)]
+    for s in (1, 4, 3):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        alone = [gu.host_bits(x) for x in _run(ua, q[lo:hi], k[lo:hi], v[lo:hi], do[lo:hi],
+                                                np.array([0, hi - lo], dtype=np.int32))]
+        for a, b in zip(batch, alone):
+            assert np.array_equal(a[lo:hi], b), s
+    # reversed order
+    order = [4, 3, 2, 1, 0]
+    parts = [(int(cu[s]), int(cu[s + 1])) for s in order]
+    cat = lambda x: np.concatenate([x[lo:hi] for lo, hi in parts])
+    cu2 = inputs.cu_seqlens([hi - lo for lo, hi in parts])
+    rev = [gu.host_bits(x) for x in _run(ua, cat(q), cat(k), cat(v), cat(do), cu2)]
+    for j, (lo, hi) in enumerate(parts):
+        for a, b in zip(batch, rev):
+            assert np.array_equal(a[lo:hi], b[int(cu2[j]):int(cu2[j + 1])])
+
+
+def test_sum_of_key_gradients_is_small(ua):
+    """The keys' dK of one (sequence, kv head) sum to zero exactly in the
+    definition; the GPU's sum stays within the accumulated bound."""
+    q, k, v, do, cu = _inputs([400, 97], 8, 2, 128, 1.0, 3)
+    _, dk, _ = _run(ua, q, k, v, do, cu)
+    _, sk, _ = oracle.backward_error_scales(q, k, v, do, cu)
+    got = gu.host_f64(dk)
+    for b in range(2):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        tot = np.abs(got[lo:hi].sum(axis=0))
+        assert np.all(tot <= (A_COEF + R_COEF) * sk[lo:hi].sum(axis=0)), b
