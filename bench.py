@@ -162,6 +162,11 @@ def main():
     steps = uattn.DecodeSteps(q_steps, kp, vp, table_dev, seqlens_steps, L, out_steps)
     out_prompt = torch.empty_like(qp)
     out_full = torch.empty_like(q)
+    lse_full = torch.empty((q.shape[0], hq), dtype=torch.float32, device=dev)
+    # policy-update backward: upstream gradient ~ N(0,1), gradient buffers and workspace
+    dout = inputs.normal_bf16_device(tuple(q.shape), 1.0, 7, 3)
+    dq_b, dk_b, dv_b = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    bwd_ws = torch.empty(uattn.prefill_backward_workspace_bytes(q.shape[0], hq), dtype=torch.uint8, device=dev)
     # log-prob leg: one row per response token
     rows = B * R
     # LM head: hidden states [rows, Hq*d] ~ N(0,1) and weights ~ N(0, sigma^2/H), so the
@@ -216,8 +221,12 @@ def main():
         uattn.qk_norm_rope(q, k, pos_full, qn_w, kn_w, cos_sin, q_out=q_rope, k_out=k_rope)
         ev["nr"].b.record()
         ev["upd"].a.record()
-        uattn.prefill(q, k, v, cu_dev, L, out=out_full)
+        uattn.prefill(q, k, v, cu_dev, L, out=out_full, lse=lse_full)
         ev["upd"].b.record()
+        ev["bwd"].a.record()
+        uattn.prefill_backward(q, k, v, out_full, dout, lse_full, cu_dev, L, dq=dq_b, dk=dk_b, dv=dv_b,
+                               workspace=bwd_ws)
+        ev["bwd"].b.record()
         ev["lm"].a.record()
         uattn.lm_head(hidden, lm_w, out=logits)
         ev["lm"].b.record()
@@ -227,7 +236,7 @@ def main():
 
     def new_events():
         return {"pre": Ev(torch), "kvw": Ev(torch), "nr": Ev(torch), "upd": Ev(torch), "lm": Ev(torch),
-                "lp": Ev(torch), "dec": Ev(torch)}
+                "lp": Ev(torch), "dec": Ev(torch), "bwd": Ev(torch)}
 
     for i in range(args.warmup):
         step(new_events())
@@ -245,6 +254,7 @@ def main():
     K = args.steps
     pre_ms = sum(e["pre"].ms() for e in evs) / K
     upd_ms = sum(e["upd"].ms() for e in evs) / K
+    bwd_ms = sum(e["bwd"].ms() for e in evs) / K
     lp_ms = sum(e["lp"].ms() for e in evs) / K
     kvw_ms = sum(e["kvw"].ms() for e in evs) / K
     nr_ms = sum(e["nr"].ms() for e in evs) / K
@@ -258,6 +268,9 @@ def main():
     dec_bytes = w.decode_kv_bytes()
     lp_bytes = float(rows) * V * 2
     upd_tflops = upd_flop / (upd_ms * 1e-3) / 1e12
+    # backward: five products per causal (query, key) pair (S recomputed, dP, dV, dK, dQ) = 2.5 x forward
+    bwd_flop = 2.5 * upd_flop
+    bwd_tflops = bwd_flop / (bwd_ms * 1e-3) / 1e12
     pre_tflops = pre_flop / (pre_ms * 1e-3) / 1e12
     dec_gbs_wall = dec_bytes / (dec_wall_ms * 1e-3) / 1e9
     lp_gbs = lp_bytes / (lp_ms * 1e-3) / 1e9
@@ -339,9 +352,21 @@ def main():
             "flop_per_launch": upd_flop,
             "avg_launch_ms": round(upd_ms, 4),
         },
+        "roofline_backward": {
+            "kernel": "uattn_prefill_backward (bwd_prep + bwd_dkdv + bwd_dq over 8 x 4096)",
+            "bound": "mfma",
+            "achieved": round(bwd_tflops, 2),
+            "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(bwd_tflops / BF16_PEAK_TFLOPS, 4),
+            "flop_per_call": bwd_flop,
+            "flop_is": "5 products x 2*d FLOP per causal (query, key) pair per q head (2.5 x the forward)",
+            "avg_call_ms": round(bwd_ms, 4),
+        },
         "phases_ms": {"prompt_prefill": round(pre_ms, 4), "kv_write": round(kvw_ms, 4), "decode": round(dec_wall_ms, 3),
                       "qk_norm_rope": round(nr_ms, 4), "lm_head": round(lm_ms, 4),
-                      "update_prefill": round(upd_ms, 4), "logprob": round(lp_ms, 4)},
+                      "update_prefill": round(upd_ms, 4), "update_backward": round(bwd_ms, 4),
+                      "logprob": round(lp_ms, 4)},
         "prompt_prefill_tflops": round(pre_tflops, 2),
         "logprob_gbs": round(lp_gbs, 2),
         "logprob_frac_hbm": round(lp_gbs / HBM_PEAK_GBS, 4),

@@ -123,9 +123,12 @@ def backward_error_scales(q: np.ndarray, k: np.ndarray, v: np.ndarray, dout: np.
 
 
 def dq_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, dout: np.ndarray, cu_seqlens: Sequence[int],
-                 rows: Iterable[Tuple[int, int]], scale: Optional[float] = None) -> np.ndarray:
+                 rows: Iterable[Tuple[int, int]], scale: Optional[float] = None, with_scale: bool = False):
     """dQ at chosen (packed token index, q head) rows, each from its own row's
-    data and its sequence's keys and values: dQ_i = scale sum_j P_ij (dO_i.V_j - dO_i.O_i) K_j."""
+    data and its sequence's keys and values: dQ_i = scale sum_j P_ij (dO_i.V_j - dO_i.O_i) K_j.
+
+    With ``with_scale`` also returns the rows' error magnitudes (the sq of
+    backward_error_scales, from the same row data)."""
     rows = list(rows)
     hq, hkv, d = q.shape[1], k.shape[1], q.shape[2]
     g = hq // hkv
@@ -133,6 +136,7 @@ def dq_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, dout: np.ndarray, 
         scale = default_scale(d)
     cu = np.asarray(cu_seqlens, dtype=np.int64)
     out = np.zeros((len(rows), d), dtype=np.float64)
+    mag = np.zeros((len(rows), d), dtype=np.float64)
     for r, (t, h) in enumerate(rows):
         b = int(np.searchsorted(cu, t, side="right") - 1)
         lo = int(cu[b])
@@ -146,4 +150,7 @@ def dq_rows_fp64(q: np.ndarray, k: np.ndarray, v: np.ndarray, dout: np.ndarray, 
         dp = vj @ doi
         ds = p * (dp - np.dot(doi, p @ vj))
         out[r] = scale * (ds @ kj)
-    return out
+        if with_scale:
+            a = np.dot(np.abs(doi), p @ np.abs(vj))
+            mag[r] = scale * ((np.abs(ds) + a * p) @ np.abs(kj))
+    return (out, mag) if with_scale else out

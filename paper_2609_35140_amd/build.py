@@ -50,20 +50,51 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(resource_usage: bool = False, out: str = LIB, verbose: bool = False, defines=()) -> str:
-    cmd = [hipcc(), *COMMON_FLAGS, *[f"-D{d}" for d in defines], "-shared", f"-I{INCLUDE}", f"-I{CSRC}", *sources(),
-           "-o", out + ".tmp"]
+# Extra flags for single sources.  The backward's dK/dV kernel carries 128 fp32
+# accumulators through its loop; by default the compiler parks them in AGPRs
+# and copies them to VGPRs and back on every iteration (about 200 moves per
+# 128 MFMAs).  Asking for the VGPR form of the MFMAs removes the copies.  Only
+# this file: the flag changes the decode kernel's code too.
+PER_FILE_FLAGS = {
+    "uattn_backward.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+OBJDIR = os.path.join(PKG, "_build")
+
+
+def _compile(src: str, defines, resource_usage: bool):
+    obj = os.path.join(OBJDIR, os.path.basename(src)[:-4] + ".o")
+    cmd = [hipcc(), *COMMON_FLAGS, *PER_FILE_FLAGS.get(os.path.basename(src), []), *[f"-D{d}" for d in defines],
+           f"-I{INCLUDE}", f"-I{CSRC}", "-c", src, "-o", obj]
     if resource_usage:
         cmd.insert(1, "-Rpass-analysis=kernel-resource-usage")
-    if verbose:
-        print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
+    return obj, cmd, res
+
+
+def build(resource_usage: bool = False, out: str = LIB, verbose: bool = False, defines=()) -> str:
+    """Compile every source to its own object (in parallel), then link the library."""
+    from concurrent.futures import ThreadPoolExecutor
+    os.makedirs(OBJDIR, exist_ok=True)
+    srcs = sources()
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        results = list(ex.map(lambda f: _compile(f, defines, resource_usage), srcs))
+    for obj, cmd, res in results:
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            raise RuntimeError(f"hipcc failed with code {res.returncode} on {os.path.basename(obj)}")
+        if resource_usage:
+            lines = [ln for ln in res.stderr.splitlines() if "remark" in ln]
+            sys.stdout.write("\n".join(lines) + "\n")
+    link = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *[obj for obj, _, _ in results], "-o", out + ".tmp"]
+    if verbose:
+        print(" ".join(link), flush=True)
+    res = subprocess.run(link, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with code {res.returncode}")
-    if resource_usage:
-        lines = [ln for ln in res.stderr.splitlines() if "remark" in ln or "Function Name" in ln or ":" in ln]
-        sys.stdout.write("\n".join(lines) + "\n")
+        raise RuntimeError(f"link failed with code {res.returncode}")
     os.replace(out + ".tmp", out)
     return out
 

@@ -26,6 +26,8 @@
 // Both products of dS and P with Q, dO or K take their transposed operand
 // from the transposing LDS read (ds_read_b64_tr_b16); all tiles move by
 // direct-to-LDS loads with explicit wait counts, as in the forward.
+#include <type_traits>
+
 #include "uattn_internal.h"
 #include "uattn_numerics.h"
 #include "uattn_tile_io.h"
@@ -33,17 +35,21 @@
 namespace uattn {
 namespace {
 
-// One [64 rows][D] bf16 tile in LDS, read two ways: row fragments (8
-// consecutive rows at one 16-byte piece per 128-byte LDS cycle) and
-// transposing reads (4 consecutive rows x 2 adjacent pieces).  The XOR
-// swizzle ((row & 3) << 1 | (row >> 2) & 1) puts both patterns on distinct
-// banks: 8 consecutive rows take 8 distinct values, and 4 consecutive rows
-// take distinct values of bits 1-2 (the piece pair).
+// One [64 rows][D] bf16 tile in LDS, read two ways: row fragments
+// (ds_read_b128, a 16-lane group reads 16 consecutive rows at one logical
+// 16-byte piece) and transposing reads (ds_read_b64_tr_b16, a 16-lane group
+// reads 4 consecutive rows x 2 adjacent pieces; 32 lanes share an LDS cycle).
+// The 16-byte pieces of each row are XOR-swizzled by 2 * (row & 7).  For
+// d = 128 this was measured with the LDS bank-conflict counter on gfx950: it
+// leaves both patterns conflict-free, while swizzles that spread 16 rows over
+// 16 distinct pieces conflict on one pattern or the other.  For d = 64, whose
+// 128-byte rows pair up in a 256-byte bank line, the same permutation is
+// applied to row pairs (2 * ((row >> 1) & 3)).
 template <int D>
 struct BwdTile {
   static constexpr int kPieces = D / 8;
   static constexpr int kElems = kTileKeys * D;
-  __device__ __forceinline__ static int swz(int row) { return ((row & 3) << 1) | ((row >> 2) & 1); }
+  __device__ __forceinline__ static int swz(int row) { return D == 128 ? 2 * (row & 7) : 2 * ((row >> 1) & 3); }
   __device__ __forceinline__ static int off(int row, int piece) { return row * D + 8 * (piece ^ swz(row)); }
 };
 
@@ -79,7 +85,7 @@ template <int D>
 __device__ __forceinline__ void read_tr_operand(const __bf16* tile, int db, int lane, bf16x8 (&a)[2]) {
   using BT = BwdTile<D>;
   const int g = lane >> 4, src = lane & 15;
-  const int row = 4 * g + (src >> 2);  // + 32*st + 16*h, which leave the swizzle unchanged
+  const int row = 4 * g + (src >> 2);  // + 32*st + 16*h: bits 4-5, which the swizzle ignores
   const int sub = src & 3;
   const int piece = (2 * db + (sub >> 1)) ^ BT::swz(row);
   const __bf16* base = tile + row * D + 8 * piece + 4 * (sub & 1);
@@ -190,7 +196,8 @@ __global__ __launch_bounds__(kKvWaves * 64, 1) void bwd_dkdv_kernel(BwdParams p)
   const int k0 = kt * kKeyTile;
   if (k0 >= L) return;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int g = lane >> 4, col = lane & 15;
   const int kw0 = k0 + kKeysPerWave * wave;
 
@@ -279,26 +286,32 @@ __global__ __launch_bounds__(kKvWaves * 64, 1) void bwd_dkdv_kernel(BwdParams p)
 
     // P and dS = P (dP - D); keys after the query, and rows past the
     // sequence, get P = 0
-    const bool full = (q0 >= kw0 + kKeysPerWave - 1) && (q0 + kQTile <= L);
+    const bool full = (q0 >= kw0 + kKeysPerWave - 1) && (q0 + kQTile <= L);  // wave-uniform
     float pv[2][4][4], dsv[2][4][4];
+    auto weights = [&](auto masked) {
 #pragma unroll
-    for (int qb = 0; qb < 4; ++qb) {
-      const f32x4 l2 = *reinterpret_cast<const f32x4*>(lvec + 16 * qb + 4 * g);
-      const f32x4 dd = *reinterpret_cast<const f32x4*>(dvec + 16 * qb + 4 * g);
+      for (int qb = 0; qb < 4; ++qb) {
+        const f32x4 l2 = *reinterpret_cast<const f32x4*>(lvec + 16 * qb + 4 * g);
+        const f32x4 dd = *reinterpret_cast<const f32x4*>(dvec + 16 * qb + 4 * g);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float x = hw_exp2(__builtin_fmaf(s[qb][nb][j], c, -l2[j]));
-          if (!full) {
-            const int qp = q0 + 16 * qb + 4 * g + j;
-            const int kp = kw0 + 16 * nb + col;
-            x = (kp <= qp && qp < L) ? x : 0.f;
+          for (int j = 0; j < 4; ++j) {
+            float x = hw_exp2(__builtin_fmaf(s[qb][nb][j], c, -l2[j]));
+            if constexpr (decltype(masked)::value) {
+              const int qp = q0 + 16 * qb + 4 * g + j;
+              const int kp = kw0 + 16 * nb + col;
+              x = (kp <= qp && qp < L) ? x : 0.f;
+            }
+            pv[nb][qb][j] = x;
+            dsv[nb][qb][j] = x * (dp[qb][nb][j] - dd[j]);
           }
-          pv[nb][qb][j] = x;
-          dsv[nb][qb][j] = x * (dp[qb][nb][j] - dd[j]);
-        }
-    }
+      }
+    };
+    if (full)
+      weights(std::false_type{});
+    else
+      weights(std::true_type{});
     bf16x8 pb[2][2], sb[2][2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
@@ -370,7 +383,8 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
   const int qt = nqt - 1 - zrev;
   if (qt < 0) return;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int g = lane >> 4, col = lane & 15;
   const int q0 = qt * kDqRows + wave * kDqWaveRows;
   const bool wave_on = q0 < L;
@@ -447,6 +461,7 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
         }
       }
       bf16x8 sb[kDqNB][2];
+      const bool diag = t == my_last_tile;  // wave-uniform: only this tile holds keys after a query
 #pragma unroll
       for (int nb = 0; nb < kDqNB; ++nb) {
         const int qp = q0 + kQCols * nb + col;
@@ -456,7 +471,7 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             float x = hw_exp2(__builtin_fmaf(s[nb][kb][j], c, -l2v[nb]));
-            if (t == my_last_tile) x = (t * kTileKeys + score_key(kb, j, g) > qp) ? 0.f : x;
+            if (diag) x = (t * kTileKeys + score_key(kb, j, g) > qp) ? 0.f : x;
             dsv[kb][j] = x * (dp[nb][kb][j] - ddv[nb]);
           }
         pack_rows(dsv, sb[nb]);

@@ -130,3 +130,60 @@ def test_sum_of_key_gradients_is_small(ua):
         lo, hi = int(cu[b]), int(cu[b + 1])
         tot = np.abs(got[lo:hi].sum(axis=0))
         assert np.all(tot <= (A_COEF + R_COEF) * sk[lo:hi].sum(axis=0)), b
+
+
+def test_full_size_qwen_gqa(ua):
+    """The benchmark shape (8 x 4096 tokens, 32 q / 8 kv heads, d 128, N(0,0.25)
+    inputs, N(0,1) upstream gradient), in the launch configuration the
+    benchmark times: 256 sampled dQ rows and one whole (sequence, kv head) of
+    dK and dV against the oracle, and one sequence run alone equal bit for
+    bit to its rows in the batch."""
+    import torch
+    cfg = pytest.importorskip("config_util")
+    w = inputs.qwen_gqa()
+    pk = cfg.DevicePack(w, tag=106)
+    hq, hkv, d = w.num_q_heads, w.num_kv_heads, w.head_dim
+    grp = hq // hkv
+    dout = inputs.normal_bf16_device(tuple(pk.q.shape), 1.0, 106, 9)
+    out, lse = ua.prefill(pk.q, pk.k, pk.v, pk.cu_dev, pk.max_seqlen, return_lse=True)
+    dq, dk, dv = ua.prefill_backward(pk.q, pk.k, pk.v, out, dout, lse, pk.cu_dev, pk.max_seqlen)
+    torch.cuda.synchronize()
+
+    def seq_host(s):
+        lo, hi = int(pk.cu[s]), int(pk.cu[s + 1])
+        return lo, hi, [gu.host_bits(x[lo:hi]) for x in (pk.q, pk.k, pk.v, dout)]
+
+    g = inputs.rng(51, 0)
+    picks = {}
+    for _ in range(256):
+        picks.setdefault(int(g.integers(0, w.num_seqs)), []).append(
+            (int(g.integers(0, w.seq_lens[0])), int(g.integers(0, hq))))
+    got, ref, mag = [], [], []
+    dq_bits = gu.host_bits(dq)
+    for s, rows in sorted(picks.items()):
+        lo, hi, (qs, ks, vs, ds) = seq_host(s)
+        r, m = oracle.dq_rows_fp64(qs, ks, vs, ds, [0, hi - lo], rows, with_scale=True)
+        ref.append(r)
+        mag.append(m)
+        got.append(np.stack([dq_bits[lo + p, h] for p, h in rows]))
+    print("full size, 256 sampled rows:", flush=True)
+    _check("dq", np.concatenate(got), np.concatenate(ref), np.concatenate(mag))
+
+    s, kvh = 3, 5
+    lo, hi, (qs, ks, vs, ds) = seq_host(s)
+    heads = list(range(kvh * grp, (kvh + 1) * grp))
+    args = (qs[:, heads], ks[:, kvh:kvh + 1], vs[:, kvh:kvh + 1], ds[:, heads], [0, hi - lo])
+    _, rk, rv = oracle.attention_backward_fp64(*args)
+    _, sk, sv = oracle.backward_error_scales(*args)
+    print(f"full size, sequence {s}, kv head {kvh}, all {hi - lo} keys:", flush=True)
+    _check("dk", gu.host_bits(dk)[lo:hi, kvh:kvh + 1], rk, sk)
+    _check("dv", gu.host_bits(dv)[lo:hi, kvh:kvh + 1], rv, sv)
+
+    s = 6
+    lo, hi = int(pk.cu[s]), int(pk.cu[s + 1])
+    cu1 = gu.dev_i32([0, hi - lo])
+    sl = [x[lo:hi].contiguous() for x in (pk.q, pk.k, pk.v, dout)]
+    o1, l1 = ua.prefill(sl[0], sl[1], sl[2], cu1, hi - lo, return_lse=True)
+    alone = ua.prefill_backward(sl[0], sl[1], sl[2], o1, sl[3], l1, cu1, hi - lo)
+    for a, b in zip((dq, dk, dv), alone):
+        assert torch.equal(a[lo:hi].view(torch.int16), b.view(torch.int16))

@@ -149,6 +149,8 @@ def test_dq_rows_match_full_gradient():
     q, k, v, do, cu = _case(lens, 4, 2, 16, 7)
     dq, _, _ = oracle.attention_backward_fp64(q, k, v, do, cu)
     rows = [(0, 0), (29, 3), (30, 1), (94, 2), (60, 0)]
-    got = oracle.dq_rows_fp64(q, k, v, do, cu, rows)
+    got, mag = oracle.dq_rows_fp64(q, k, v, do, cu, rows, with_scale=True)
+    sq, _, _ = oracle.backward_error_scales(q, k, v, do, cu)
     for r, (t, h) in enumerate(rows):
         assert np.allclose(got[r], dq[t, h], rtol=1e-12, atol=1e-14)
+        assert np.allclose(mag[r], sq[t, h], rtol=1e-12, atol=1e-14)
