@@ -245,7 +245,7 @@ __device__ __forceinline__ void mask_block(f32x4& s, int block_base, int qpos, i
 // The online-softmax step for one block given the tile maximum: the same
 // operations, element for element, as the full-tile step.
 __device__ __forceinline__ float softmax_block(f32x4& s, float& m, float tmax, float c) {
-  const float m_new = fmaxf(m, tmax);
+  const float m_new = vmax(m, tmax);
   const float mc_old = m * c;
   const float mc_new = m_new * c;
   const float alpha = hw_exp2(mc_old - mc_new);
@@ -381,7 +381,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           if (t == last_tile) mask_block(s[nb], t * kTileKeys + 16 * wave, qpos, lane);
-          float bmax = fmaxf(fmaxf(s[nb][0], s[nb][1]), fmaxf(s[nb][2], s[nb][3]));
+          float bmax = vmax(vmax(s[nb][0], s[nb][1]), vmax(s[nb][2], s[nb][3]));
           bmax = max_xor16(bmax);
           bmax = max_xor32(bmax);
           if (g == 0) sm.xmax[nb][wave][col] = bmax;
@@ -392,8 +392,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
         float alpha[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          const float tmax = fmaxf(fmaxf(sm.xmax[nb][0][col], sm.xmax[nb][1][col]),
-                                   fmaxf(sm.xmax[nb][2][col], sm.xmax[nb][3][col]));
+          const float tmax = vmax(vmax(sm.xmax[nb][0][col], sm.xmax[nb][1][col]),
+                                  vmax(sm.xmax[nb][2][col], sm.xmax[nb][3][col]));
           alpha[nb] = softmax_block(s[nb], m[nb], tmax, c);
           bf16x4 pw;
 #pragma unroll

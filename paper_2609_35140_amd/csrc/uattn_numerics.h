@@ -87,6 +87,13 @@ struct TileLayout {
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 
+// The maximum used for every running max and block max: IEEE 754-2019
+// maximum (NaN propagates, -0 < +0), one v_maximum3_f32 per three operands.
+// The C library maximum would give the same values for the finite and -inf
+// operands compared here, but the compiler must then canonicalize each MFMA
+// result it reads (an extra v_max_f32 x, x per score).
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 __device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }
 
@@ -149,11 +156,11 @@ __device__ __forceinline__ void mask_scores(f32x4 (&s)[4], int key_base, int qpo
 // the operands in the same order in every lane.
 __device__ __forceinline__ float max_xor32(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float max_xor16(float x) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // ---------------------------------------------------------------------------
@@ -165,11 +172,11 @@ __device__ __forceinline__ float max_xor16(float x) {
 __device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float c) {
   float t[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) t[j] = fmaxf(fmaxf(s[0][j], s[1][j]), fmaxf(s[2][j], s[3][j]));
-  float tmax = fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3]));
+  for (int j = 0; j < 4; ++j) t[j] = vmax(vmax(s[0][j], s[1][j]), vmax(s[2][j], s[3][j]));
+  float tmax = vmax(vmax(t[0], t[1]), vmax(t[2], t[3]));
   tmax = max_xor16(tmax);
   tmax = max_xor32(tmax);
-  const float m_new = fmaxf(m, tmax);
+  const float m_new = vmax(m, tmax);
   const float mc_old = m * c;
   const float mc_new = m_new * c;
   const float alpha = hw_exp2(mc_old - mc_new);
@@ -257,7 +264,7 @@ struct FoldScale {
 };
 __device__ __forceinline__ FoldScale fold_scale(float M, float m, float c) {
   FoldScale f;
-  f.m_new = fmaxf(M, m);
+  f.m_new = vmax(M, m);
   const float mc_new = f.m_new * c;
   f.a = hw_exp2(M * c - mc_new);
   f.b = hw_exp2(m * c - mc_new);
