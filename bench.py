@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
+    ap.add_argument("--cpu-row-seconds", type=float, default=2.0,
+                    help="budget of each other row's CPU-oracle sample")
     ap.add_argument("--eager-decode", action="store_true", help="launch the decode steps one by one (no HIP graph)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="before timing, copy 1 GiB device to device once (the known-size dispatch that scales "
@@ -300,8 +302,10 @@ def main():
 
     # ------------------------------------------------------------------ CPU oracle baseline
     cpu = None
+    cpu_rows = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, host, table, npages, args.cpu_seconds)
+        cpu_rows = cpu_row_baselines(w, host, table, npages, args.cpu_row_seconds)
 
     dec_launch_bytes = dec_bytes / R
     dec_launch_ms = dec_kernel_ms / R
@@ -380,6 +384,7 @@ def main():
         "bitwise_rows": [n_match, n_rows],
         "logprob_batch_invariant": ratio_one,
         "cpu_baseline": cpu,
+        "cpu_baselines_other_rows": cpu_rows,
     }
     print(json.dumps(result), flush=True)
 
@@ -416,6 +421,86 @@ def cpu_baseline(w, host, table, npages, budget_s):
             "sample": f"{done_steps} of the 3072 decode steps (random order, batch 8, 32 q heads) through "
                       f"oracle.paged_decode_fp64 in {el:.1f}s on 1 thread",
             "seconds": round(el, 2)}
+
+
+def cpu_row_baselines(w, host, table, npages, budget_s):
+    """The fp64 oracle of every other row of the step on a bounded sample of the
+    same workload (one BLAS thread each), in the unit of that row's GPU figure.
+    Each row repeats its sample until `budget_s` seconds have passed."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    from paper_2609_35140_amd import inputs
+
+    hq, hkv, d, P = w.num_q_heads, w.num_kv_heads, w.head_dim, w.prompt_lens[0]
+    grp = hq // hkv
+    cu = host["cu_seqlens"]
+
+    def timed(fn):
+        n, t0 = 0, time.perf_counter()
+        while True:
+            fn()
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s:
+                return n, el
+
+    out = {}
+    with threadpool_limits(limits=1):
+        # prefill: the first 1024 positions of sequence 0, the 4 q heads of kv head 0
+        n = 1024
+        q = host["q"][:n, :grp]
+        k = host["k"][:n, :1]
+        v = host["v"][:n, :1]
+        flop = 4.0 * d * grp * n * (n + 1) / 2
+        reps, el = timed(lambda: oracle.causal_attention_fp64(q, k, v, [0, n]))
+        out["prefill"] = {"value": round(flop * reps / el / 1e12, 6), "unit": "TFLOP/s",
+                          "sample": f"oracle.causal_attention_fp64, 1 x {n} tokens x {grp} q heads, x{reps}"}
+        # backward: 512 positions, same heads, N(0,1) upstream gradient
+        n = 512
+        do = inputs.normal_bf16((n, grp, d), 1.0, 7, 3)
+        flop = 2.5 * 4.0 * d * grp * n * (n + 1) / 2
+        reps, el = timed(lambda: oracle.attention_backward_fp64(host["q"][:n, :grp], host["k"][:n, :1],
+                                                                 host["v"][:n, :1], do, [0, n]))
+        out["update_backward"] = {"value": round(flop * reps / el / 1e12, 6), "unit": "TFLOP/s",
+                                  "sample": f"oracle.attention_backward_fp64, 1 x {n} tokens x {grp} q heads, x{reps}"}
+        # LM head: 16 rows x a 8192-entry vocabulary slice x hidden Hq*d
+        H = hq * d
+        hid = inputs.normal_bf16((16, H), 1.0, 7, 4)
+        wt = inputs.normal_bf16((8192, H), w.logit_sigma / float(np.sqrt(H)), 7, 5)
+        reps, el = timed(lambda: oracle.logits_fp64(hid, wt))
+        out["lm_head"] = {"value": round(2.0 * 16 * 8192 * H * reps / el / 1e12, 6), "unit": "TFLOP/s",
+                          "sample": f"oracle.logits_fp64, 16 rows x 8192 vocab x {H}, x{reps}"}
+        # log-prob: 16 rows of the full vocabulary
+        lg = inputs.logits_bf16(16, w.vocab, w.logit_sigma, tag=9)
+        tg = inputs.targets(16, w.vocab, tag=9)
+        reps, el = timed(lambda: oracle.logprob_fp64(lg, tg))
+        out["logprob"] = {"value": round(16 * w.vocab * 2 * reps / el / 1e9, 4), "unit": "GB/s",
+                          "sample": f"oracle.logprob_fp64, 16 rows x {w.vocab}, x{reps}"}
+        # KV write: the prompt tokens of sequence 0 into a copy of the paged cache
+        kp = inputs.scatter_to_pages(host["k"], cu, table, npages, w.page_size)
+        vp = inputs.scatter_to_pages(host["v"], cu, table, npages, w.page_size)
+        kn, vn = host["k"][:P], host["v"][:P]
+        seq = np.zeros(P, dtype=np.int32)
+        pos = np.arange(P, dtype=np.int32)
+        reps, el = timed(lambda: oracle.kv_write(kp, vp, kn, vn, table, seq, pos))
+        out["kv_write"] = {"value": round(P * hkv * d * 2 * 2 * 2 * reps / el / 1e9, 4), "unit": "GB/s",
+                           "sample": f"oracle.kv_write, {P} tokens x {hkv} kv heads, x{reps}"}
+        # Q/K RMSNorm + NeoX RoPE: 256 tokens of sequence 0
+        n = 256
+        cs = oracle.rope_table(n, d, 1e6)
+        wq = inputs.normal_bf16((d,), 1.0, 90, 0)
+        wk = inputs.normal_bf16((d,), 1.0, 90, 1)
+        posn = np.arange(n)
+        reps, el = timed(lambda: (oracle.qk_norm_rope(host["q"][:n], posn, wq, 1e-6, cs),
+                                  oracle.qk_norm_rope(host["k"][:n], posn, wk, 1e-6, cs)))
+        out["qk_norm_rope"] = {"value": round(n * (hq + hkv) * d * 2 * 2 * reps / el / 1e9, 4), "unit": "GB/s",
+                               "sample": f"oracle.qk_norm_rope, {n} tokens x ({hq} + {hkv}) heads, x{reps}"}
+    for v in out.values():
+        v.update({"cores": 1, "kind": "oracle"})
+    log("cpu oracle rows: " + ", ".join(f"{k} {v['value']} {v['unit']}" for k, v in out.items()))
+    return out
 
 
 if __name__ == "__main__":
