@@ -143,6 +143,7 @@ struct Ring {
 };
 
 constexpr int64_t kLdsBytesPerCu = 160 * 1024;
+constexpr int kLenScanMax = 4096;  // batches up to this size skip chunks past their longest entry
 
 template <int D, int NB>
 struct DecodeSmem {
@@ -158,6 +159,7 @@ struct DecodeSmem {
   bf16x4 pbuf[NB][4][64];               // per key block: the bf16 weights, in the lanes' PV operand order
   int32_t pend[kMaxPend][2];            // (b * Hkv + kv head, chunk count)
   int32_t flag[kMaxPend];
+  int32_t lenmax[4];                    // per wave: the longest entry it read
 };
 
 // Issue the descriptor and query loads of candidate `cand` (chunk-major
@@ -272,9 +274,21 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, col = lane & 15;
-  const int ncand = p.batch * p.hkv * p.nchunk_max;
+  const int ncand_all = p.batch * p.hkv * p.nchunk_max;
   const int stride = gridDim.x;
   const float c = p.c;
+
+  // Chunks past the longest entry hold no work.  When this workgroup's walk
+  // is longer than the three items described at start, read the batch's
+  // lengths (the loads overlap the first descriptor fetches) and stop the
+  // walk after the last chunk any entry has, so that a max_seqlen far above
+  // the actual lengths costs no descriptor round trips for empty items.
+  int lmax = 0;
+  const bool scan = p.nchunk_max > 1 && p.batch <= kLenScanMax && ncand_all > 3 * stride;
+  if (scan) {
+#pragma unroll 4
+    for (int i = tid; i < p.batch; i += 256) lmax = max(lmax, p.seqlens[i]);
+  }
 
   int issued = 0;    // tiles whose loads were issued
   int computed = 0;  // tiles computed
@@ -283,10 +297,20 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
   int seq = 0;       // item sequence number of r0: candidate blockIdx.x + seq * stride
   Ring r0, r1, r2;
 
-  fetch_item<D, NB>(p, sm, r0, blockIdx.x, ncand, 0, issued, wave, lane);
-  fetch_item<D, NB>(p, sm, r1, blockIdx.x + stride, ncand, 1, issued, wave, lane);
-  fetch_item<D, NB>(p, sm, r2, blockIdx.x + 2 * stride, ncand, 2, issued, wave, lane);
+  fetch_item<D, NB>(p, sm, r0, blockIdx.x, ncand_all, 0, issued, wave, lane);
+  fetch_item<D, NB>(p, sm, r1, blockIdx.x + stride, ncand_all, 1, issued, wave, lane);
+  fetch_item<D, NB>(p, sm, r2, blockIdx.x + 2 * stride, ncand_all, 2, issued, wave, lane);
   wait_vmem_asm<0>();
+  int ncand = ncand_all;
+  if (scan) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) lmax = max(lmax, __shfl_xor(lmax, m));
+    if (lane == 0) sm.lenmax[wave] = lmax;
+    lds_barrier();
+    lmax = max(max(sm.lenmax[0], sm.lenmax[1]), max(sm.lenmax[2], sm.lenmax[3]));
+    const int nch = min(max((min(lmax, p.max_seqlen) + kChunkKeys - 1) / kChunkKeys, 1), p.nchunk_max);
+    ncand = __builtin_amdgcn_readfirstlane(p.batch * p.hkv * nch);
+  }
   resolve_item<D, NB>(p, sm, r0, wave);
   resolve_item<D, NB>(p, sm, r1, wave);
   resolve_item<D, NB>(p, sm, r2, wave);

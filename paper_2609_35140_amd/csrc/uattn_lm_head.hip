@@ -23,7 +23,6 @@ namespace uattn {
 namespace {
 
 constexpr int kKC = 64;       // hidden elements per chunk
-constexpr int kLmWaves = 8;
 constexpr int kLmXcds = 8;
 
 struct LmHeadParams {
@@ -38,11 +37,12 @@ struct LmHeadParams {
 // VT/WM x TT/WN), a ring of STAGES chunks.
 template <int VT, int TT, int WM, int WN, int STAGES>
 struct LmCfg {
-  static_assert(WM * WN == kLmWaves, "eight waves");
+  static constexpr int NW = WM * WN;       // waves per workgroup
   static constexpr int BI = VT / WM / 16;   // 16-row vocab blocks per wave
   static constexpr int BJ = TT / WN / 16;   // 16-column token blocks per wave
-  static constexpr int kAInstr = VT * kKC * 2 / 1024 / kLmWaves;  // 1 KB direct-to-LDS loads per wave per chunk
-  static constexpr int kBInstr = TT * kKC * 2 / 1024 / kLmWaves;
+  static constexpr int kAInstr = VT * kKC * 2 / 1024 / NW;  // 1 KB direct-to-LDS loads per wave per chunk
+  static constexpr int kBInstr = TT * kKC * 2 / 1024 / NW;
+  static_assert(kAInstr * 1024 * NW == VT * kKC * 2 && kBInstr * 1024 * NW == TT * kKC * 2, "chunk split");
   static constexpr int kChunkOps = kAInstr + kBInstr;
   struct Smem {
     __bf16 a[STAGES][VT * kKC];   // weight rows, 128 bytes each, pieces swizzled
@@ -51,7 +51,7 @@ struct LmCfg {
 };
 
 template <int VT, int TT, int WM, int WN, int STAGES>
-__global__ __launch_bounds__(kLmWaves * 64, 1) void lm_head_kernel(LmHeadParams p) {
+__global__ __launch_bounds__(WM * WN * 64, 1) void lm_head_kernel(LmHeadParams p) {
   using C = LmCfg<VT, TT, WM, WN, STAGES>;
   constexpr int BI = C::BI, BJ = C::BJ;
   __shared__ __attribute__((aligned(1024))) typename C::Smem sm;
@@ -159,7 +159,7 @@ hipError_t launch_cfg(LmHeadParams p, hipStream_t stream) {
   const int64_t nblocks = static_cast<int64_t>((p.n_vt + kLmXcds - 1) / kLmXcds) * kLmXcds * p.n_tt;
   if (nblocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((lm_head_kernel<VT, TT, WM, WN, STAGES>), dim3(static_cast<unsigned>(nblocks)),
-                     dim3(kLmWaves * 64), 0, stream, p);
+                     dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
 }
 

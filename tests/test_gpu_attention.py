@@ -263,3 +263,25 @@ def test_workspace_reuse_across_batch_sizes(ua):
         torch.cuda.synchronize()
         cnt = ws[: ua.counter_bytes(nb, 8)].view(torch.int32)
         assert int(cnt.abs().sum().item()) == 0, trial
+
+
+def test_oversized_max_seqlen_gives_the_same_bits(ua):
+    """max_seqlen far above every entry's length (a caller passing its
+    allocation size): the kernel's walk stops after the longest entry's last
+    chunk, and outputs and lse equal those with the true maximum and the
+    prefill rows bit for bit."""
+    import torch
+    w = inputs.custom(32, 8, 128, [700, 300, 1200, 90, 513, 256, 1000, 64], sigma=0.5, page_size=64)
+    pk = gu.Pack(w, seed=19, table_slack=112)          # table rows cover 8192 positions
+    out, lse = ua.prefill(pk.q, pk.k, pk.v, pk.cu_dev, pk.max_seqlen, return_lse=True)
+    rng = np.random.default_rng(23)
+    ents = [(int(s), int(rng.integers(0, w.seq_lens[s]))) for s in rng.integers(0, len(w.seq_lens), size=48)]
+    q, t, s, m, tok = pk.decode_rows(ents)
+    assert pk.table.shape[1] * pk.page >= 8192
+    big, big_lse = ua.decode(q, pk.kp, pk.vp, t, s, 8192, return_lse=True)
+    tight, tight_lse = ua.decode(q, pk.kp, pk.vp, t, s, m, return_lse=True)
+    ti = torch.from_numpy(tok).cuda()
+    assert torch.equal(big.view(torch.int16), tight.view(torch.int16))
+    assert torch.equal(big_lse.view(torch.int32), tight_lse.view(torch.int32))
+    assert torch.equal(big.view(torch.int16), out[ti].view(torch.int16))
+    assert torch.equal(big_lse.view(torch.int32), lse[ti].view(torch.int32))
