@@ -132,58 +132,91 @@ def test_sum_of_key_gradients_is_small(ua):
         assert np.all(tot <= (A_COEF + R_COEF) * sk[lo:hi].sum(axis=0)), b
 
 
-def test_full_size_qwen_gqa(ua):
-    """The benchmark shape (8 x 4096 tokens, 32 q / 8 kv heads, d 128, N(0,0.25)
-    inputs, N(0,1) upstream gradient), in the launch configuration the
-    benchmark times: 256 sampled dQ rows and one whole (sequence, kv head) of
-    dK and dV against the oracle, and one sequence run alone equal bit for
-    bit to its rows in the batch."""
+def _full_size(ua, w, tag, n_rows, full, alone):
+    """Full-size backward in the launch configuration the benchmark times:
+    n_rows sampled dQ rows against the oracle; all keys of one (sequence, kv
+    head) = `full` for dK and dV (None to skip); sequence `alone` run by
+    itself equal bit for bit to its rows in the batch."""
     import torch
     cfg = pytest.importorskip("config_util")
-    w = inputs.qwen_gqa()
-    pk = cfg.DevicePack(w, tag=106)
-    hq, hkv, d = w.num_q_heads, w.num_kv_heads, w.head_dim
+    pk = cfg.DevicePack(w, tag=tag)
+    hq, hkv = w.num_q_heads, w.num_kv_heads
     grp = hq // hkv
-    dout = inputs.normal_bf16_device(tuple(pk.q.shape), 1.0, 106, 9)
+    dout = inputs.normal_bf16_device(tuple(pk.q.shape), 1.0, tag, 9)
     out, lse = ua.prefill(pk.q, pk.k, pk.v, pk.cu_dev, pk.max_seqlen, return_lse=True)
     dq, dk, dv = ua.prefill_backward(pk.q, pk.k, pk.v, out, dout, lse, pk.cu_dev, pk.max_seqlen)
     torch.cuda.synchronize()
 
-    def seq_host(s):
+    def seq_host(s, positions=None):
+        """Host bits of sequence s: K and V in full; Q and dO in full, or only at
+        `positions` (the other rows left zero, unread by the row oracle)."""
         lo, hi = int(pk.cu[s]), int(pk.cu[s + 1])
-        return lo, hi, [gu.host_bits(x[lo:hi]) for x in (pk.q, pk.k, pk.v, dout)]
+        ks, vs = gu.host_bits(pk.k[lo:hi]), gu.host_bits(pk.v[lo:hi])
+        if positions is None:
+            return lo, hi, [gu.host_bits(pk.q[lo:hi]), ks, vs, gu.host_bits(dout[lo:hi])]
+        qs = np.zeros((hi - lo, hq, w.head_dim), dtype=np.uint16)
+        ds = np.zeros_like(qs)
+        ti = torch.from_numpy(np.array([lo + p for p in positions], dtype=np.int64)).cuda()
+        qs[positions] = gu.host_bits(pk.q[ti])
+        ds[positions] = gu.host_bits(dout[ti])
+        return lo, hi, [qs, ks, vs, ds]
 
-    g = inputs.rng(51, 0)
+    g = inputs.rng(51, tag)
     picks = {}
-    for _ in range(256):
-        picks.setdefault(int(g.integers(0, w.num_seqs)), []).append(
-            (int(g.integers(0, w.seq_lens[0])), int(g.integers(0, hq))))
+    for _ in range(n_rows):
+        s = int(g.integers(0, w.num_seqs))
+        picks.setdefault(s, []).append((int(g.integers(0, w.seq_lens[s])), int(g.integers(0, hq))))
     got, ref, mag = [], [], []
-    dq_bits = gu.host_bits(dq)
     for s, rows in sorted(picks.items()):
-        lo, hi, (qs, ks, vs, ds) = seq_host(s)
+        lo, hi, (qs, ks, vs, ds) = seq_host(s, sorted({p for p, _ in rows}))
         r, m = oracle.dq_rows_fp64(qs, ks, vs, ds, [0, hi - lo], rows, with_scale=True)
+        ti = torch.from_numpy(np.array([lo + p for p, _ in rows], dtype=np.int64)).cuda()
+        bits = gu.host_bits(dq[ti])
         ref.append(r)
         mag.append(m)
-        got.append(np.stack([dq_bits[lo + p, h] for p, h in rows]))
-    print("full size, 256 sampled rows:", flush=True)
+        got.append(np.stack([bits[i, h] for i, (_, h) in enumerate(rows)]))
+        del qs, ks, vs, ds
+    print(f"{w.name}: {n_rows} sampled dQ rows:", flush=True)
     _check("dq", np.concatenate(got), np.concatenate(ref), np.concatenate(mag))
 
-    s, kvh = 3, 5
-    lo, hi, (qs, ks, vs, ds) = seq_host(s)
-    heads = list(range(kvh * grp, (kvh + 1) * grp))
-    args = (qs[:, heads], ks[:, kvh:kvh + 1], vs[:, kvh:kvh + 1], ds[:, heads], [0, hi - lo])
-    _, rk, rv = oracle.attention_backward_fp64(*args)
-    _, sk, sv = oracle.backward_error_scales(*args)
-    print(f"full size, sequence {s}, kv head {kvh}, all {hi - lo} keys:", flush=True)
-    _check("dk", gu.host_bits(dk)[lo:hi, kvh:kvh + 1], rk, sk)
-    _check("dv", gu.host_bits(dv)[lo:hi, kvh:kvh + 1], rv, sv)
+    if full is not None:
+        s, kvh = full
+        lo, hi, (qs, ks, vs, ds) = seq_host(s)
+        heads = list(range(kvh * grp, (kvh + 1) * grp))
+        args = (qs[:, heads], ks[:, kvh:kvh + 1], vs[:, kvh:kvh + 1], ds[:, heads], [0, hi - lo])
+        _, rk, rv = oracle.attention_backward_fp64(*args)
+        _, sk, sv = oracle.backward_error_scales(*args)
+        print(f"{w.name}: sequence {s}, kv head {kvh}, all {hi - lo} keys:", flush=True)
+        _check("dk", gu.host_bits(dk[lo:hi, kvh:kvh + 1]), rk, sk)
+        _check("dv", gu.host_bits(dv[lo:hi, kvh:kvh + 1]), rv, sv)
 
-    s = 6
-    lo, hi = int(pk.cu[s]), int(pk.cu[s + 1])
+    lo, hi = int(pk.cu[alone]), int(pk.cu[alone + 1])
     cu1 = gu.dev_i32([0, hi - lo])
     sl = [x[lo:hi].contiguous() for x in (pk.q, pk.k, pk.v, dout)]
     o1, l1 = ua.prefill(sl[0], sl[1], sl[2], cu1, hi - lo, return_lse=True)
-    alone = ua.prefill_backward(sl[0], sl[1], sl[2], o1, sl[3], l1, cu1, hi - lo)
-    for a, b in zip((dq, dk, dv), alone):
+    one = ua.prefill_backward(sl[0], sl[1], sl[2], o1, sl[3], l1, cu1, hi - lo)
+    for a, b in zip((dq, dk, dv), one):
         assert torch.equal(a[lo:hi].view(torch.int16), b.view(torch.int16))
+    print(f"{w.name}: sequence {alone} ({hi - lo} tokens) alone == in the batch, bit for bit", flush=True)
+
+
+def test_full_size_qwen_gqa(ua):
+    """Benchmark shape: 8 x 4096 tokens, 32 q / 8 kv heads, d 128, N(0,0.25)
+    inputs, N(0,1) upstream gradient."""
+    _full_size(ua, inputs.qwen_gqa(), 106, 256, (3, 5), 6)
+
+
+def test_full_size_varlen_pack(ua):
+    """Varlen training pack: 64 sequences ~U[512, 8192] (278K tokens), 40 q /
+    8 kv heads (group 5), N(0,1) inputs; dK/dV in full for the shortest
+    sequence."""
+    w = inputs.varlen_pack()
+    short = int(np.argmin(w.seq_lens))
+    _full_size(ua, w, 107, 256, (short, 3), int(np.argmax(w.seq_lens)))
+
+
+def test_full_size_long_context(ua):
+    """Long context: 8 x 32768 tokens, 64 q / 8 kv heads (group 8), N(0,0.25)
+    inputs: sampled dQ rows (dK/dV of a 32K sequence is beyond the oracle's
+    budget here) and one 32K sequence alone == in the batch."""
+    _full_size(ua, inputs.long_context(), 108, 64, None, 2)
