@@ -299,6 +299,12 @@ def main():
     ratio_one = bool(torch.equal(lp_sub.view(torch.int32), logp[sub].view(torch.int32)))
     del ua_rows
     log(f"bitwise rows {n_match}/{n_rows}; logprob batch-invariant: {ratio_one}")
+    # the backward is deterministic: a second call into fresh buffers gives the same bits
+    grads2 = uattn.prefill_backward(q, k, v, out_full, dout, lse_full, cu_dev, L, workspace=bwd_ws)
+    bwd_repeat = all(bool(torch.equal(a.view(torch.int16), b.view(torch.int16)))
+                     for a, b in zip((dq_b, dk_b, dv_b), grads2))
+    del grads2
+    log(f"backward repeat bitwise equal: {bwd_repeat}")
 
     # ------------------------------------------------------------------ CPU oracle baseline
     cpu = None
@@ -383,6 +389,7 @@ def main():
         "bitwise_match_pct": round(bitwise_pct, 4),
         "bitwise_rows": [n_match, n_rows],
         "logprob_batch_invariant": ratio_one,
+        "backward_repeat_bitwise": bwd_repeat,
         "cpu_baseline": cpu,
         "cpu_baselines_other_rows": cpu_rows,
     }

@@ -258,10 +258,11 @@ __device__ __forceinline__ float softmax_block(f32x4& s, float& m, float tmax, f
 }
 
 // The load stream of a workgroup: the tiles of its items, in item order,
-// into a four-stage LDS ring, with the descriptor and query loads of the item
-// two ahead interleaved in the same stream.  Loads of one wave complete in
-// issue order, so "tile k has landed" also means "everything this wave
-// issued before tile k has landed"; that is the only fact the waits rely on.
+// into the LDS tile ring (two stages for d = 128, four for d = 64), with the
+// descriptor and query loads of the item two ahead interleaved in the same
+// stream.  Loads of one wave complete in issue order, so "tile k has landed"
+// also means "everything this wave issued before tile k has landed"; that is
+// the only fact the waits rely on.
 template <int D, int NB>
 __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
   using TL = TileLayout<D>;

@@ -1,14 +1,13 @@
 // Full-sequence entry point: causal GQA attention over a packed varlen batch.
 //
-// Workgroup = 8 waves = 128 consecutive query rows of one q head of one
-// sequence; wave w owns rows q0 .. q0+15 (q0 = tile*128 + 16*w), one row per
-// MFMA column.  Two waves share each SIMD, so one wave's matrix work overlaps
-// the other's softmax.  All waves stream the same K/V tiles through LDS
-// stages filled by direct-to-LDS loads; a wave stops at its own diagonal tile
-// (q0 / 64), so no row ever sees a tile without a visible key.  Every row's
-// arithmetic is the shared per-tile sequence in uattn_numerics.h,
-// chunk-folded every 4 tiles, exactly as the decode path folds its
-// positional split.
+// Workgroup = 8 waves = 256 consecutive query rows of one q head of one
+// sequence; wave w owns rows q0 .. q0+31 (q0 = tile*256 + 32*w), two 16-column
+// MFMA blocks, one row per column.  Two waves share each SIMD.  All waves
+// stream the same K/V tiles through a two-stage LDS ring filled by
+// direct-to-LDS loads; a wave stops at its own diagonal tile (q0 / 64), so no
+// row ever sees a tile without a visible key.  Every row's arithmetic is the
+// shared per-tile sequence in uattn_numerics.h, chunk-folded every 4 tiles,
+// exactly as the decode path folds its positional split.
 //
 // Grid: one dimension; see the workgroup-id mapping below (query tiles counted
 // from the END of each sequence, so the longest work is dispatched first, and
@@ -76,7 +75,8 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
   const int qt = nqt - 1 - zrev;
   if (qt < 0) return;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int g = lane >> 4, col = lane & 15;
   const int q0 = qt * kWgRows + wave * kWaveRows;
   const bool wave_on = q0 < L;
