@@ -220,3 +220,41 @@ def test_full_size_long_context(ua):
     inputs: sampled dQ rows (dK/dV of a 32K sequence is beyond the oracle's
     budget here) and one 32K sequence alone == in the batch."""
     _full_size(ua, inputs.long_context(), 108, 64, None, 2)
+
+
+def test_graph_replay_with_varying_inputs(ua):
+    """The forward and backward captured in one HIP graph, replayed with new
+    inputs written into the captured buffers, with eager work between the
+    replays: every replay equals the eager calls bit for bit."""
+    import torch
+    lens = [300, 129, 1, 513]
+    hq, hkv, d = 8, 2, 128
+    cu = inputs.cu_seqlens(lens)
+    T = int(cu[-1])
+    cud = gu.dev_i32(cu)
+    bufs = [torch.empty((T, h, d), dtype=torch.bfloat16, device="cuda") for h in (hq, hkv, hkv, hq)]
+    q, k, v, do = bufs
+    ws = torch.empty(ua.prefill_backward_workspace_bytes(T, hq), dtype=torch.uint8, device="cuda")
+    out = torch.empty_like(q)
+    lse = torch.empty((T, hq), dtype=torch.float32, device="cuda")
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=s):
+            ua.prefill(q, k, v, cud, 513, out=out, lse=lse, stream=s)
+            ua.prefill_backward(q, k, v, out, do, lse, cud, 513, dq=dq, dk=dk, dv=dv, workspace=ws, stream=s)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for i, b in enumerate(bufs):
+            b.copy_(gu.dev(inputs.normal_bf16(tuple(b.shape), 1.0, 82, rep, i)))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        o2, l2 = ua.prefill(q, k, v, cud, 513, return_lse=True)
+        e = ua.prefill_backward(q, k, v, o2, do, l2, cud, 513)
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), o2.view(torch.int16)), rep
+        for a, b in zip((dq, dk, dv), e):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), rep
