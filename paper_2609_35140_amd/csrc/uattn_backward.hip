@@ -143,17 +143,24 @@ __device__ __forceinline__ void seq_range(const BwdParams& p, int seq, int& lo, 
 
 // ---------------------------------------------------------------------------
 // D_i = dO_i . O_i (fp32, lane-ordered partial sums then an xor butterfly) and
-// lse_i * log2(e), for every (token, q head) row.  D/8 lanes per row.
+// lse_i * log2(e), for every (token, q head) row.  D/8 lanes per row.  Rows
+// are enumerated head-major (r = h * T + t), the order of the two workspace
+// planes, so consecutive rows write consecutive words (each row's out and
+// dout reads are one 2*D-byte run either way).
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
   constexpr int LPR = D / 8;
   constexpr int kRows = 256 / LPR;
   const int64_t rows = static_cast<int64_t>(p.total) * p.hq;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * kRows + threadIdx.x / LPR;
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * kRows + threadIdx.x / LPR;
   const int sub = threadIdx.x % LPR;
+  int64_t row = 0;  // token-major index of (t, h) in out, dout and lse
   float acc = 0.f;
-  if (row < rows) {
+  if (r < rows) {
+    const int h = static_cast<int>(r / p.total);
+    const int64_t t = r % p.total;
+    row = t * p.hq + h;
     const bf16x8 o = *reinterpret_cast<const bf16x8*>(p.out + row * D + 8 * sub);
     const bf16x8 d = *reinterpret_cast<const bf16x8*>(p.dout + row * D + 8 * sub);
 #pragma unroll
@@ -161,12 +168,9 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
   }
 #pragma unroll
   for (int m = LPR / 2; m >= 1; m >>= 1) acc = acc + __shfl_xor(acc, m, LPR);
-  if (row < rows && sub == 0) {
-    const int64_t t = row / p.hq;
-    const int h = static_cast<int>(row % p.hq);
-    const int64_t dst = static_cast<int64_t>(h) * p.total + t;
-    p.ws_d[dst] = acc;
-    p.ws_l2[dst] = p.lse[row] * 1.44269504088896340736f;
+  if (r < rows && sub == 0) {
+    p.ws_d[r] = acc;
+    p.ws_l2[r] = p.lse[row] * 1.44269504088896340736f;
   }
 }
 
