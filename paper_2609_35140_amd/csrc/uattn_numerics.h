@@ -164,26 +164,40 @@ __device__ __forceinline__ float max_xor16(float x) {
 }
 
 // ---------------------------------------------------------------------------
-// Online-softmax step of one query column for one tile.  In: raw scores s
-// (masked).  Out: s holds p = exp2(fma(s, c, -m_new*c)); m updated; returns
-// alpha = exp2(m_old*c - m_new*c).  The row sum l is accumulated by the PV
-// product (pv_tile), from the same bf16 p that weights V.
+// Online-softmax step of one query column for one tile, in three pieces that
+// every kernel composes in the same order:
+//   tile_max      the column maximum of the (masked) raw scores of the tile,
+//                 in every lane of the column;
+//   rescale_alpha alpha = exp2(m_old*c - m_new*c) with m_new = max(m_old, tile max);
+//   tile_weights  s <- p = exp2(fma(s, c, -m_new*c)).
+// The row sum l is accumulated by the PV product (pv_tile), from the same
+// bf16 p that weights V.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float c) {
+__device__ __forceinline__ float tile_max(const f32x4 (&s)[4]) {
   float t[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) t[j] = vmax(vmax(s[0][j], s[1][j]), vmax(s[2][j], s[3][j]));
   float tmax = vmax(vmax(t[0], t[1]), vmax(t[2], t[3]));
   tmax = max_xor16(tmax);
-  tmax = max_xor32(tmax);
-  const float m_new = vmax(m, tmax);
-  const float mc_old = m * c;
+  return max_xor32(tmax);
+}
+__device__ __forceinline__ float rescale_alpha(float m_old, float m_new, float c) {
+  const float mc_old = m_old * c;
   const float mc_new = m_new * c;
-  const float alpha = hw_exp2(mc_old - mc_new);
+  return hw_exp2(mc_old - mc_new);
+}
+__device__ __forceinline__ void tile_weights(f32x4 (&s)[4], float m_new, float c) {
+  const float mc_new = m_new * c;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
     for (int j = 0; j < 4; ++j) s[kb][j] = hw_exp2(__builtin_fmaf(s[kb][j], c, -mc_new));
+}
+// The whole step: s <- p, m <- m_new; returns alpha.
+__device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float c) {
+  const float m_new = vmax(m, tile_max(s));
+  const float alpha = rescale_alpha(m, m_new, c);
+  tile_weights(s, m_new, c);
   m = m_new;
   return alpha;
 }
@@ -210,20 +224,20 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
 // lsum[nb] <- alpha[nb] * lsum + 1^T P_nb^T: the same product with an all-ones
 // operand in place of V^T, so every register of lsum holds the column's
 // running sum of the bf16 weights (l).
-//   stage  : LDS stage holding the V tile (TileLayout)
+//   vtile  : LDS V tile, [64 keys][D] with the TileLayout V swizzle
 // The V^T operand of step st for d block db (lane i of group g: row d = 16*db + i,
 // keys 32*st + 16*h + 4*g + k for the two halves h) comes from two transposing
 // reads whose source lane s addresses key (32*st + 16*h + 4*g + s/4), column
 // 16*db + 4*(s%4).
 template <int D, int NB, int NDB>
-__device__ __forceinline__ void pv_tile(const __bf16* stage, const bf16x8 (&pb)[NB][2], f32x4 (&acc)[NB][NDB],
+__device__ __forceinline__ void pv_tile(const __bf16* vtile, const bf16x8 (&pb)[NB][2], f32x4 (&acc)[NB][NDB],
                                         f32x4 (&lsum)[NB], const float (&alpha)[NB], int db0, int lane) {
   using TL = TileLayout<D>;
   const int g = lane >> 4, src = lane & 15;
   const int key = 4 * g + (src >> 2);       // + 32*st + 16*half; the swizzle depends on key bits below 16
   const int swz = TL::v_swz(key);
   const int sub = src & 3;                  // 4-column group inside the 16-wide d block
-  const __bf16* vrow = stage + TL::kTileElems + key * D + 4 * (sub & 1);
+  const __bf16* vrow = vtile + key * D + 4 * (sub & 1);
   bf16x8 ones;
 #pragma unroll
   for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);

@@ -147,7 +147,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
         alpha[nb] = softmax_tile(s[nb], m[nb], c);
         pack_p(s[nb], pb[nb]);
       }
-      pv_tile<D, kNB, NDB>(stage, pb, acc, lsum, alpha, 0, lane);
+      pv_tile<D, kNB, NDB>(stage + TL::kTileElems, pb, acc, lsum, alpha, 0, lane);
       if (t == my_last_tile || (t % kTilesPerChunk) == kTilesPerChunk - 1) {
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) {
