@@ -12,6 +12,7 @@
 // Grid: one dimension; see the workgroup-id mapping below (query tiles counted
 // from the END of each sequence, so the longest work is dispatched first, and
 // the q heads sharing a kv head kept on one XCD).
+#include <type_traits>
 #include "uattn_internal.h"
 #include "uattn_numerics.h"
 #include "uattn_tile_io.h"
@@ -129,8 +130,9 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
 #pragma unroll
   for (int t = 0; t < kStages - 1; ++t)
     if (t <= wg_last_tile) issue_tile(t);
-  for (int t = 0; t <= wg_last_tile; ++t) {
-    __bf16* stage = lds + (t % kStages) * TL::kStageElems;
+  auto tile_step = [&](int t, auto stage_const) {  // tile t, in stage SI = t % kStages
+    constexpr int SI = decltype(stage_const)::value;
+    __bf16* stage = lds + SI * TL::kStageElems;
     // this wave's rows of tile t are in LDS once only the later tiles' loads
     // remain; after the barrier every wave's rows are, and every wave is done
     // with tile t-1
@@ -172,6 +174,13 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
         }
       }
     }
+  };
+  // The tile loop is unrolled by the stage count, so that every LDS address
+  // of a stage is a constant offset from one base (no per-tile address math).
+  static_assert(kStages == 2, "unrolled by the stage count");
+  for (int t = 0; t <= wg_last_tile; t += 2) {
+    tile_step(t, std::integral_constant<int, 0>{});
+    if (t + 1 <= wg_last_tile) tile_step(t + 1, std::integral_constant<int, 1>{});
   }
 
 #pragma unroll
