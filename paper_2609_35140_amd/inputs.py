@@ -188,6 +188,22 @@ def packed_qkv(w: Workload, seed: int = BASE_SEED, tag: int = 0) -> Dict[str, np
     }
 
 
+def ramp_keys(t: Dict[str, np.ndarray], growth: float) -> Dict[str, np.ndarray]:
+    """The same pack with every key row of a sequence scaled by
+    (1 + position / growth) and rounded back to bf16: scores then grow along
+    the sequence, so an online softmax meets tile maxima far above the ones
+    before them (a stress case for the rescaling path)."""
+    cu = t["cu_seqlens"]
+    k = bf16_bits_to_f32(t["k"]).copy()
+    for b in range(len(cu) - 1):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        f = (1.0 + np.arange(hi - lo, dtype=np.float32) / np.float32(growth)).astype(np.float32)
+        k[lo:hi] *= f[:, None, None]
+    out = dict(t)
+    out["k"] = np.ascontiguousarray(f32_to_bf16_bits(k))
+    return out
+
+
 def paged_layout(seq_lens: Sequence[int], page_size: int, seed: int = BASE_SEED, tag: int = 0,
                  extra_pages: int = 0, max_pages_per_seq: Optional[int] = None) -> Tuple[np.ndarray, int]:
     """A block table [B, maxp] (int32) over a shuffled pool of physical pages.

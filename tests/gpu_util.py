@@ -40,10 +40,13 @@ def rows_equal_bits(a: np.ndarray, b: np.ndarray) -> np.ndarray:
 class Pack:
     """A packed varlen batch on the GPU plus its paged cache."""
 
-    def __init__(self, w, seed=42, tag=0, page_size=None, fill_bits=0x7FC0, extra_pages=5, table_slack=8):
+    def __init__(self, w, seed=42, tag=0, page_size=None, fill_bits=0x7FC0, extra_pages=5, table_slack=8,
+                 key_ramp=None):
         from paper_2609_35140_amd import inputs
         self.w = w
         t = inputs.packed_qkv(w, seed=seed, tag=tag)
+        if key_ramp is not None:
+            t = inputs.ramp_keys(t, key_ramp)
         self.host = t
         self.cu = t["cu_seqlens"]
         self.q, self.k, self.v = dev(t["q"]), dev(t["k"]), dev(t["v"])

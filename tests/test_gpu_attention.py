@@ -78,6 +78,28 @@ def test_decode_every_position_bitwise_equals_prefill(ua, name, mk, seed):
     assert oracle.parity_report(gu.host_f64(dout), o64)["pass"]
 
 
+def test_rising_scores_rescale_path(ua):
+    """Keys growing along the sequence make the online softmax's running
+    maximum jump inside and across chunks (large rescales and fold factors):
+    the prefill meets the oracle gate and every decoded position equals its
+    prefill row bit for bit, lse included."""
+    w = inputs.custom(8, 2, 128, [700, 300, 65], sigma=0.5, page_size=64)
+    pk = gu.Pack(w, seed=42, key_ramp=8.0)
+    out, lse = _prefill(ua, pk)
+    o64, lse64 = oracle.causal_attention_fp64(pk.host["q"], pk.host["k"], pk.host["v"], pk.cu)
+    rep = oracle.parity_report(gu.host_f64(out), o64)
+    print("rising scores", rep, flush=True)
+    assert rep["pass"], rep
+    lg = lse.cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(lg - lse64)) < oracle.LSE_ABS
+    entries = [(s, p) for s, L in enumerate(w.seq_lens) for p in range(L)]
+    q, table, seqlens, maxs, tok = pk.decode_rows(entries)
+    dout, dlse = ua.decode(q, pk.kp, pk.vp, table, seqlens, maxs, return_lse=True)
+    eq = gu.rows_equal_bits(gu.host_bits(dout), gu.host_bits(out)[tok])
+    assert eq.all(), f"{(~eq).sum()} of {eq.size} rows differ"
+    assert np.array_equal(dlse.cpu().numpy().view(np.uint32), lse.cpu().numpy()[tok].view(np.uint32))
+
+
 def test_rollout_replay_eq1(ua):
     """Eq. (1): full prefill of p||y equals prefill(p) at prompt rows and
     token-by-token decode (batch of all sequences each step) at response rows."""

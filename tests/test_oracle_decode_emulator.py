@@ -139,3 +139,24 @@ def test_parity_gate_rejects_one_ulp_bias_everywhere():
     bits = oracle.to_bf16_bits(o32).astype(np.int32)
     shifted = oracle.bf16_to_f64((bits + 1).astype(np.uint16))
     assert not oracle.parity_report(shifted, o64)["pass"]
+
+
+def test_emulator_rising_scores_move_the_reference_within_gate():
+    """Keys growing along the sequence push tile maxima far above the earlier
+    ones (by more than 2^8 in the exp2 domain, inside and across chunks), so
+    the rescale and fold paths carry real weight; the emulation still meets
+    the gate against the fp64 definition, lse included."""
+    w = inputs.custom(2, 1, 64, [700, 200], sigma=0.5)
+    t = inputs.ramp_keys(inputs.packed_qkv(w), 16.0)
+    qf, kf = oracle.bf16_to_f64(t["q"]), oracle.bf16_to_f64(t["k"])
+    c = (1.0 / 8.0) * oa.LOG2E
+    s = kf[:700, 0] @ qf[699, 0]
+    tmax = [s[i:i + 64].max() for i in range(0, 700, 64)]
+    jumps = [(tmax[i] - max(tmax[:i])) * c for i in range(1, len(tmax))]
+    assert max(jumps) > 8.0, jumps   # the stress is real
+    o64, lse64 = oracle.causal_attention_fp64(t["q"], t["k"], t["v"], t["cu_seqlens"])
+    o32, lse32 = oracle.tile_emulate_fp32(t["q"], t["k"], t["v"], t["cu_seqlens"])
+    rep = oracle.parity_report(o32, o64)
+    assert rep["pass"], rep
+    assert np.max(np.abs(lse32 - lse64)) < oracle.LSE_ABS
+
