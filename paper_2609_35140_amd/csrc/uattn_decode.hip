@@ -73,6 +73,14 @@ __device__ __forceinline__ void st_coherent(float* p, float v) {
 __device__ __forceinline__ float ld_coherent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// 16 bytes per lane with the same device-coherent cache policy (sc1) as the
+// scalar stores above, through a buffer resource: one store instruction per
+// four partial values instead of four, and lanes whose offset lies past the
+// resource's size store nothing.
+constexpr int kCoherentPolicy = 16;  // the sc1 bit of the buffer instructions' cache-policy operand
+__device__ __forceinline__ void st_coherent16(__amdgpu_buffer_rsrc_t r, int voffset, const f32x4& v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voffset, 0, kCoherentPolicy);
+}
 
 // Fold the chunk partials of entry b, kv head kvh (all its q heads) in chunk
 // order and write the normalized outputs.  Called by the workgroup that
@@ -169,7 +177,8 @@ struct Item {
 };
 
 template <int D, int NB>
-__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
+__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const int32_t* __restrict__ seqlens,
+                                                        const int32_t* __restrict__ block_table) {
   using TL = TileLayout<D>;
   using SM = DecodeSmem<D, NB>;
   constexpr int KS = D / 32;                   // K steps of the score product
@@ -207,9 +216,9 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
 
   // An item's descriptor, for this wave: the entry length and the page of
   // each 16-key block of the wave's tile (table index clamped, so
-  // speculative).  Wave-uniform loads, so they take the scalar path and do not
-  // queue behind the vector loads of the K/V stream; the next item's are read
-  // an item ahead.
+  // speculative).  Wave-uniform loads of read-only arguments, so they are
+  // scalar loads, counted apart from the vector loads and stores; the next
+  // item's are issued before the current item's operand loads.
   struct Desc {
     int len;
     int page[kKeyBlocks];
@@ -217,8 +226,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
   auto load_desc = [&](int it) -> Desc {
     Desc d;
     const int chunk = it / per_chunk, b = (it % per_chunk) / p.hkv;
-    const int32_t* row = p.bt + static_cast<int64_t>(b) * p.maxp;
-    d.len = p.seqlens[b];
+    const int32_t* row = block_table + static_cast<int64_t>(b) * p.maxp;
+    d.len = seqlens[b];
 #pragma unroll
     for (int kb = 0; kb < kKeyBlocks; ++kb) {
       const int pos = (chunk * kTilesPerChunk + wave) * kTileKeys + 16 * kb;
@@ -412,18 +421,18 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p) {
           if (p.lse != nullptr && wave == 0 && g == 0) p.lse[orow] = finalize_lse(m_end[nb], lsum[nb][0], c);
         }
       } else {
+        // the group's partial rows of this chunk: [head gi][chunk][d], heads
+        // past the group fall outside the resource and store nothing
+        const int64_t slot0 = (static_cast<int64_t>(cur.b) * p.hq + cur.kvh * p.group) * p.nchunk_max;
+        const auto racc = buffer_rsrc(p.ws_acc + slot0 * D, p.group * p.nchunk_max * D * 4);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           const int gi = kQCols * nb + col;
-          if (gi >= p.group) continue;
-          const int64_t ws_slot =
-              (static_cast<int64_t>(cur.b) * p.hq + cur.kvh * p.group + gi) * p.nchunk_max + cur.chunk;
-          float* arow = p.ws_acc + ws_slot * D + 16 * wave * NDBW + 4 * g;
+          const int voff = ((gi * p.nchunk_max + cur.chunk) * D + 16 * wave * NDBW + 4 * g) * 4;
 #pragma unroll
-          for (int db = 0; db < NDBW; ++db)
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) st_coherent(arow + 16 * db + jj, acc[nb][db][jj]);
-          if (wave == 0 && g == 0) {
+          for (int db = 0; db < NDBW; ++db) st_coherent16(racc, voff + 64 * db, acc[nb][db]);
+          if (gi < p.group && wave == 0 && g == 0) {
+            const int64_t ws_slot = slot0 + static_cast<int64_t>(gi) * p.nchunk_max + cur.chunk;
             st_coherent(p.ws_ml + ws_slot * 2, m_end[nb]);
             st_coherent(p.ws_ml + ws_slot * 2 + 1, lsum[nb][0]);
           }
@@ -488,7 +497,7 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
     const int64_t per_cu = 2 * smem_bytes + 1024 <= kLdsBytesPerCu ? 2 : 1;
     const int64_t slots = per_cu * a.num_cus;
     const dim3 grid(static_cast<unsigned>(ncand < slots ? ncand : slots));
-    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, p, p.seqlens, p.bt);
   };
   if (a.head_dim == 128) {
     if (two)
