@@ -139,13 +139,15 @@ __device__ __forceinline__ void qk_scores(const __bf16* stage, const bf16x8 (&qf
   }
 }
 
-// Select -inf for keys after the query: key position key_base + key > qpos.
+// Select -inf for keys after the query: key position key_base + key > qpos,
+// i.e. 16*kb + j > qpos - key_base - 4*g, one bound per lane compared with
+// constants.
 __device__ __forceinline__ void mask_scores(f32x4 (&s)[4], int key_base, int qpos, int lane) {
-  const int g = lane >> 4;
+  const int bound = qpos - key_base - 4 * (lane >> 4);
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) s[kb][j] = (key_base + score_key(kb, j, g) > qpos) ? neg_inf() : s[kb][j];
+    for (int j = 0; j < 4; ++j) s[kb][j] = (score_key(kb, j, 0) > bound) ? neg_inf() : s[kb][j];
 }
 
 // Cross-group reductions with the gfx950 lane-swap instructions.  With both
@@ -229,7 +231,12 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
 // keys 32*st + 16*h + 4*g + k for the two halves h) comes from two transposing
 // reads whose source lane s addresses key (32*st + 16*h + 4*g + s/4), column
 // 16*db + 4*(s%4).
-template <int D, int NB, int NDB>
+//
+// kFirst: the first tile of a chunk, where acc and lsum are zero and alpha is
+// zero (the running maximum starts at -inf), so alpha * acc is +0 and the
+// products start from a zero accumulator instead: the same bits for finite
+// scores, without the multiplies.
+template <int D, int NB, int NDB, bool kFirst = false>
 __device__ __forceinline__ void pv_tile(const __bf16* vtile, const bf16x8 (&pb)[NB][2], f32x4 (&acc)[NB][NDB],
                                         f32x4 (&lsum)[NB], const float (&alpha)[NB], int db0, int lane) {
   using TL = TileLayout<D>;
@@ -243,8 +250,12 @@ __device__ __forceinline__ void pv_tile(const __bf16* vtile, const bf16x8 (&pb)[
   for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
+    if constexpr (kFirst) {
+      lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    } else {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) lsum[nb][j] = alpha[nb] * lsum[nb][j];
+      for (int j = 0; j < 4; ++j) lsum[nb][j] = alpha[nb] * lsum[nb][j];
+    }
 #pragma unroll
     for (int st = 0; st < 2; ++st) lsum[nb] = mfma16(ones, pb[nb][st], lsum[nb]);
   }
@@ -261,8 +272,12 @@ __device__ __forceinline__ void pv_tile(const __bf16* vtile, const bf16x8 (&pb)[
     }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
+      if constexpr (kFirst) {
+        acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[nb][db][j] = alpha[nb] * acc[nb][db][j];
+        for (int j = 0; j < 4; ++j) acc[nb][db][j] = alpha[nb] * acc[nb][db][j];
+      }
 #pragma unroll
       for (int st = 0; st < 2; ++st) acc[nb][db] = mfma16(a[st], pb[nb][st], acc[nb][db]);
     }

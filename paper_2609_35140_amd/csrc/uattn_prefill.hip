@@ -130,8 +130,10 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
 #pragma unroll
   for (int t = 0; t < kStages - 1; ++t)
     if (t <= wg_last_tile) issue_tile(t);
-  auto tile_step = [&](int t, auto stage_const) {  // tile t, in stage SI = t % kStages
+  // tile t, in stage SI = t % kStages, at position POS = t % 4 of its chunk
+  auto tile_step = [&](int t, auto stage_const, auto pos_const) {
     constexpr int SI = decltype(stage_const)::value;
+    constexpr int POS = decltype(pos_const)::value;
     __bf16* stage = lds + SI * TL::kStageElems;
     // this wave's rows of tile t are in LDS once only the later tiles' loads
     // remain; after the barrier every wave's rows are, and every wave is done
@@ -149,8 +151,9 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
         alpha[nb] = softmax_tile(s[nb], m[nb], c);
         pack_p(s[nb], pb[nb]);
       }
-      pv_tile<D, kNB, NDB>(stage + TL::kTileElems, pb, acc, lsum, alpha, 0, lane);
-      if (t == my_last_tile || (t % kTilesPerChunk) == kTilesPerChunk - 1) {
+      // a chunk's first tile starts its accumulators afresh (pv_tile kFirst)
+      pv_tile<D, kNB, NDB, POS == 0>(stage + TL::kTileElems, pb, acc, lsum, alpha, 0, lane);
+      if (t == my_last_tile || POS == kTilesPerChunk - 1) {
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) {
           if (t < kTilesPerChunk) {
@@ -167,20 +170,20 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
               for (int j = 0; j < 4; ++j) A[nb][db][j] = fold_val(f, A[nb][db][j], acc[nb][db][j]);
             M[nb] = f.m_new;
           }
-          m[nb] = neg_inf();
-          lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+          m[nb] = neg_inf();  // acc and lsum restart at the next chunk's first tile
         }
       }
     }
   };
-  // The tile loop is unrolled by the stage count, so that every LDS address
-  // of a stage is a constant offset from one base (no per-tile address math).
-  static_assert(kStages == 2, "unrolled by the stage count");
-  for (int t = 0; t <= wg_last_tile; t += 2) {
-    tile_step(t, std::integral_constant<int, 0>{});
-    if (t + 1 <= wg_last_tile) tile_step(t + 1, std::integral_constant<int, 1>{});
+  // The tile loop is unrolled by a chunk (4 tiles, two rounds of the stage
+  // ring), so that every LDS address of a stage is a constant offset from one
+  // base and a tile's place in its chunk is known at compile time.
+  static_assert(kStages == 2 && kTilesPerChunk == 4, "unrolled by a chunk of two stage rounds");
+  for (int t = 0; t <= wg_last_tile; t += 4) {
+    tile_step(t, std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
+    if (t + 1 <= wg_last_tile) tile_step(t + 1, std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{});
+    if (t + 2 <= wg_last_tile) tile_step(t + 2, std::integral_constant<int, 0>{}, std::integral_constant<int, 2>{});
+    if (t + 3 <= wg_last_tile) tile_step(t + 3, std::integral_constant<int, 1>{}, std::integral_constant<int, 3>{});
   }
 
 #pragma unroll
