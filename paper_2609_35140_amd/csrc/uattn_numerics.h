@@ -299,7 +299,10 @@ __device__ __forceinline__ FoldScale fold_scale(float M, float m, float c) {
   f.b = hw_exp2(m * c - mc_new);
   return f;
 }
-__device__ __forceinline__ float fold_val(const FoldScale& f, float X, float x) { return f.a * X + f.b * x; }
+// a*X + b*x with one rounding for the sum: fma(a, X, b*x)
+__device__ __forceinline__ float fold_val(const FoldScale& f, float X, float x) {
+  return __builtin_fmaf(f.a, X, f.b * x);
+}
 
 // Final normalization and the optional log-sum-exp (natural log, scaled scores).
 __device__ __forceinline__ __bf16 finalize_val(float A, float L) { return to_bf16(A / L); }

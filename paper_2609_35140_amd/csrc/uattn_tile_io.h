@@ -84,6 +84,14 @@ __device__ __forceinline__ void dma_b128(const void* src, uint32_t lds_wave_base
                : "v"(src), "s"(lds_wave_base)
                : "memory", "m0");
 }
+// The same from a wave-uniform base plus a per-lane 32-bit byte offset (the
+// instruction's scalar-base form: no 64-bit address arithmetic per lane).
+__device__ __forceinline__ void dma_b128_based(const void* sbase, uint32_t voffset, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voffset), "s"(sbase), "s"(lds_wave_base)
+               : "memory", "m0");
+}
 // 4 bytes per lane from `src` to LDS at m0 + 4*lane.
 __device__ __forceinline__ void dma_b32(const void* src, uint32_t lds_wave_base) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
@@ -128,6 +136,21 @@ __device__ __forceinline__ void load_tile_rows_async(__bf16* stage, const __bf16
   static_assert(kInstr >= 1 && RPW * TL::kPieces == 64 * kInstr, "tile split");
   const __bf16* zero = reinterpret_cast<const __bf16*>(g_zero_rows) + 8 * (lane & 15);
   const uint32_t kd0 = __builtin_amdgcn_readfirstlane(lds_addr(stage + wave * kInstr * 64 * 8));
+  if (nvalid >= RPW) {
+    // every row of this wave is in the sequence: uniform bases, per-lane
+    // byte offsets that do not change from tile to tile
+#pragma unroll
+    for (int i = 0; i < kInstr; ++i) {
+      const int slot = (wave * kInstr + i) * 64 + lane;
+      const int row = slot / TL::kPieces, piece = slot % TL::kPieces;
+      const int r = row - RPW * wave;
+      const uint32_t ko = static_cast<uint32_t>((r * row_stride + 8 * (piece ^ TL::k_swz(row))) * 2);
+      const uint32_t vo = static_cast<uint32_t>((r * row_stride + 8 * (piece ^ TL::v_swz(row))) * 2);
+      dma_b128_based(kbase, ko, kd0 + i * 64 * 16);
+      dma_b128_based(vbase, vo, kd0 + i * 64 * 16 + TL::kTileElems * 2);
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < kInstr; ++i) {
     const int slot = (wave * kInstr + i) * 64 + lane;
