@@ -64,6 +64,20 @@ __device__ __forceinline__ void load_pair_async(__bf16* dst, const __bf16* abase
   static_assert(kInstr >= 1 && RPW * BT::kPieces == 64 * kInstr, "tile split");
   const __bf16* zero = reinterpret_cast<const __bf16*>(g_zero_rows) + 8 * (lane & 15);
   const uint32_t d0 = __builtin_amdgcn_readfirstlane(lds_addr(dst + wave * kInstr * 64 * 8));
+  if (nvalid >= RPW) {
+    // every row of this wave is in the sequence: uniform bases and per-lane
+    // byte offsets that do not change from tile to tile
+#pragma unroll
+    for (int i = 0; i < kInstr; ++i) {
+      const int slot = (wave * kInstr + i) * 64 + lane;
+      const int row = slot / BT::kPieces, piece = slot % BT::kPieces;
+      const int r = row - RPW * wave;
+      const uint32_t o = static_cast<uint32_t>((r * row_stride + 8 * (piece ^ BT::swz(row))) * 2);
+      dma_b128_based(abase, o, d0 + i * 1024);
+      dma_b128_based(bbase, o, d0 + i * 1024 + BT::kElems * 2);
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < kInstr; ++i) {
     const int slot = (wave * kInstr + i) * 64 + lane;  // 16-byte LDS piece of the tile
@@ -259,11 +273,12 @@ __global__ __launch_bounds__(kKvWaves * 64, 1) void bwd_dkdv_kernel(BwdParams p)
   const float c = p.c;
 
   issue(0);
-  for (int it = 0; it < n; ++it) {
+  auto step = [&](int it, auto stage_const) {  // step it, in stage SI = it % 2
+    constexpr int SI = decltype(stage_const)::value;
     // stage it has landed in every wave, and every wave is done with stage it-1
     wait_barrier<0>();
     if (it + 1 < n) issue(it + 1);
-    const __bf16* qs = lds + (it & 1) * kStageElems;
+    const __bf16* qs = lds + SI * kStageElems;
     const __bf16* dos = qs + BT::kElems;
     const float* dvec = reinterpret_cast<const float*>(qs + 2 * BT::kElems);
     const float* lvec = dvec + 64;
@@ -337,6 +352,11 @@ __global__ __launch_bounds__(kKvWaves * 64, 1) void bwd_dkdv_kernel(BwdParams p)
         for (int st = 0; st < 2; ++st) dk_acc[db][nb] = mfma16(qtr[st], sb[nb][st], dk_acc[db][nb]);
       }
     }
+  };
+  // unrolled by the stage count: stage addresses are constant offsets
+  for (int it = 0; it < n; it += 2) {
+    step(it, std::integral_constant<int, 0>{});
+    if (it + 1 < n) step(it + 1, std::integral_constant<int, 1>{});
   }
 
   // lane (g, col): key kw0 + 16*nb + col, d = 16*db + 4*g .. +3
@@ -440,11 +460,12 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
   const float c = p.c;
 
   issue(0);
-  for (int t = 0; t <= wg_last_tile; ++t) {
+  auto tile_step = [&](int t, auto stage_const) {  // tile t, in stage SI = t % 2
+    constexpr int SI = decltype(stage_const)::value;
     wait_barrier<0>();
     if (t + 1 <= wg_last_tile) issue(t + 1);
     if (wave_on && t <= my_last_tile) {
-      const __bf16* ks = lds + (t & 1) * kStageElems;
+      const __bf16* ks = lds + SI * kStageElems;
       const __bf16* vs = ks + BT::kElems;
       // S^T = K Q^T and dP^T = V dO^T: rows = keys 16*kb + 4*g + j, column = query 16*nb + col
       f32x4 s[kDqNB][4], dp[kDqNB][4];
@@ -468,14 +489,15 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
       const bool diag = t == my_last_tile;  // wave-uniform: only this tile holds keys after a query
 #pragma unroll
       for (int nb = 0; nb < kDqNB; ++nb) {
-        const int qp = q0 + kQCols * nb + col;
+        // key t*64 + 16*kb + 4*g + j is after the query iff 16*kb + j > bound
+        const int bound = q0 + kQCols * nb + col - t * kTileKeys - 4 * g;
         float dsv[4][4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             float x = hw_exp2(__builtin_fmaf(s[nb][kb][j], c, -l2v[nb]));
-            if (diag) x = (t * kTileKeys + score_key(kb, j, g) > qp) ? 0.f : x;
+            if (diag) x = (score_key(kb, j, 0) > bound) ? 0.f : x;
             dsv[kb][j] = x * (dp[nb][kb][j] - ddv[nb]);
           }
         pack_rows(dsv, sb[nb]);
@@ -491,6 +513,11 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
           for (int st = 0; st < 2; ++st) acc[nb][db] = mfma16(kt[st], sb[nb][st], acc[nb][db]);
       }
     }
+  };
+  // unrolled by the stage count: stage addresses are constant offsets
+  for (int t = 0; t <= wg_last_tile; t += 2) {
+    tile_step(t, std::integral_constant<int, 0>{});
+    if (t + 1 <= wg_last_tile) tile_step(t + 1, std::integral_constant<int, 1>{});
   }
 
 #pragma unroll
