@@ -307,9 +307,9 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
 #pragma unroll
           for (int st = 0; st < KS; ++st) qf[nb][st] = buffer_load16(rq, q_off + nb * kQCols * D * 2 + 64 * st, 0);
       }
+      int64_t boff[kKeyBlocks];  // element offset of key 16*kb of the tile in the pools, -1 if none
+      int rows[kKeyBlocks];      // keys of block kb inside the context
       if (tile_on) {
-        int64_t boff[kKeyBlocks];  // element offset of key 16*kb of the tile in the pools, -1 if none
-        int rows[kKeyBlocks];      // keys of block kb inside the context
 #pragma unroll
         for (int kb = 0; kb < kKeyBlocks; ++kb) {
           const int pos = tile * kTileKeys + 16 * kb;
@@ -321,16 +321,6 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
           const auto rk = buffer_rsrc(p.kp + (ok ? boff[kb] : 0), rows[kb] * D * 2);
 #pragma unroll
           for (int st = 0; st < KS; ++st) kf[kb][st] = buffer_load16(rk, k_off + 64 * st, 0);
-        }
-        const uint32_t vbase = __builtin_amdgcn_readfirstlane(lds_addr(&sm.v[wave][0]));
-#pragma unroll
-        for (int i = 0; i < kVInstr; ++i) {
-          const int slot = i * 64 + lane;
-          const int row = slot / TL::kPieces, piece = slot % TL::kPieces;
-          const int kb = (i * kRowsPerInstr) / 16;
-          const bool ok = (row & 15) < rows[kb];
-          const __bf16* src = ok ? p.vp + boff[kb] + (row & 15) * D + 8 * (piece ^ TL::v_swz(row)) : zero + 8 * (lane & 15);
-          dma_b128(src, vbase + i * 64 * 16);
         }
       }
 
@@ -352,6 +342,18 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
           if (tile == last_tile) mask_scores(s[nb], tile * kTileKeys, cur.n - 1, lane);
           const float tm = tile_max(s[nb]);
           if (g == 0) sm.tmax[wave][nb][col] = tm;
+        }
+        // V rows into LDS slot `wave` once the scores are formed, so that
+        // the K rows had the memory system to themselves
+        const uint32_t vbase = __builtin_amdgcn_readfirstlane(lds_addr(&sm.v[wave][0]));
+#pragma unroll
+        for (int i = 0; i < kVInstr; ++i) {
+          const int slot = i * 64 + lane;
+          const int row = slot / TL::kPieces, piece = slot % TL::kPieces;
+          const int kb = (i * kRowsPerInstr) / 16;
+          const bool ok = (row & 15) < rows[kb];
+          const __bf16* src = ok ? p.vp + boff[kb] + (row & 15) * D + 8 * (piece ^ TL::v_swz(row)) : zero + 8 * (lane & 15);
+          dma_b128(src, vbase + i * 64 * 16);
         }
       }
       lds_barrier();
