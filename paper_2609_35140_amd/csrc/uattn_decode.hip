@@ -6,11 +6,12 @@
 // workgroup take the chunk's four 64-key tiles, one each:
 //
 //   1. wave w loads the K rows of tile w straight into its score-product
-//      operand registers (no LDS), the V rows of tile w into LDS slot w
-//      (direct-to-LDS), and the query operands;
+//      operand registers (no LDS) and the query operands;
 //   2. wave w computes the scores of tile w -- the same product, mask and
-//      tile maximum as the full-sequence kernel -- and publishes the column
-//      maxima in LDS;
+//      tile maximum as the full-sequence kernel -- publishes the column
+//      maxima in LDS, and only then copies the V rows of tile w into LDS
+//      slot w (direct-to-LDS), so that the K rows meet a memory system
+//      without the V stream;
 //   3. after one barrier every wave forms the running maxima of the chunk's
 //      tiles in order (max is exact, so this is the sequential online-softmax
 //      maximum), wave w turns its tile into bf16 weights against its running
