@@ -1,26 +1,35 @@
 #!/usr/bin/env python3
 """Benchmark of the unified-attention hot path on one MI355X.
 
-One step = one pass of the whole path over one batch of the Qwen-style GQA
-workload (8 sequences of 1024 prompt + 3072 response tokens, 32 q / 8 kv
-heads, head_dim 128, bf16 ~ N(0, 0.25), paged KV with 64-token pages):
+Headline workload: long context, 8 sequences of 32,768 tokens (31,744
+prompt + 1,024 decoded), 64 q / 8 kv heads, head_dim 128, bf16 ~ N(0, 0.25),
+paged KV with 64-token pages, log-prob over a 151,936-entry vocabulary.
+One step = one pass of the whole path over that batch:
 
-  1. rollout prefill over the 8 prompts             (full-sequence entry point)
+  1. rollout prefill over the 8 prompts            (full-sequence entry point)
      and the indexed write of the prompts' K/V into the paged cache
-  2. rollout decode of the 3072 response tokens,
-     token by token, batch 8, against the paged cache (token-wise entry point)
-  3. Q/K RMSNorm + NeoX RoPE over the 8 full trajectories, then the policy-update
-     prefill over them (full-sequence entry point; it runs on the raw Q/K so
-     that the bitwise comparison with the decode rows uses the same inputs)
-  4. the batch-invariant LM head (hidden 4096 -> 151,936 logits, ~ N(0, 4)) of
-     the 8 x 3072 response tokens, and their log-probabilities
+  2. rollout decode of the 1024 response tokens, token by token, batch 8,
+     against the paged cache (token-wise entry point; the 1024 launches are
+     replayed as one HIP graph captured before timing)
+  3. Q/K RMSNorm + NeoX RoPE over the 8 full trajectories, then the
+     policy-update prefill over them (full-sequence entry point) and its
+     backward
+  4. the batch-invariant LM head (hidden 8192 -> 151,936 logits) of the
+     8 x 1024 response tokens, and their log-probabilities
 
-Inputs are resident in HBM before the timed region.  Every phase is bracketed
-by HIP events on the stream it runs on; the 3072 decode launches are replayed
-as one HIP graph captured before timing.  After timing, the decoded
-rows and the prompt-prefill rows are compared bit for bit with the policy-
-update prefill rows at the same positions (the paper's Eq. (1) at operator
-level).  The CPU oracle is timed on a bounded sample of the same decode work.
+Attention everywhere runs on the normalized, rotated Q/K (the rotated K is
+what the paged cache holds and the decode queries are the rotated rows), so
+the bitwise comparison covers the chain norm/RoPE -> attention in both
+regimes.  Inputs are resident in HBM before the timed region.  Every phase
+is bracketed by HIP events on the stream it runs on.  After timing, every
+decoded row is compared bit for bit with the policy-update prefill row at
+the same position (the paper's Eq. (1) at operator level), and the prompt
+rows of the rollout prefill with the same rows of the full prefill.
+
+Secondary figures in the same line: the Qwen-style GQA workload (8 x 4096,
+32/8 heads; decode phase and prefill), the varlen training pack and the GRPO
+rollout's full-pack prefill, measured streaming-read and MFMA ceilings, and
+the CPU oracle timed on the host's cores.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -29,7 +38,9 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import subprocess
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -50,10 +61,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="long_context", choices=["long_context", "qwen_gqa"],
+                    help="headline workload (long_context is the reported one; qwen_gqa for profiling comparisons)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-oracle sample")
-    ap.add_argument("--cpu-row-seconds", type=float, default=2.0,
-                    help="budget of each other row's CPU-oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of each CPU-oracle sample")
+    ap.add_argument("--no-secondary", action="store_true", help="skip the Qwen-style, varlen-pack and GRPO figures")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the measured-ceiling microbenchmarks")
     ap.add_argument("--eager-decode", action="store_true", help="launch the decode steps one by one (no HIP graph)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="before timing, copy 1 GiB device to device once (the known-size dispatch that scales "
@@ -62,7 +75,6 @@ def parse():
 
 
 DECODE_SOURCES = ("uattn_decode.hip", "uattn_numerics.h", "uattn_tile_io.h")
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_kernel_qwen_gqa_traffic.md")
 
 
 def decode_source_digest() -> str:
@@ -74,11 +86,12 @@ def decode_source_digest() -> str:
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per decode launch from the committed counter summary, or None
-    when it is absent or was taken on other kernel sources."""
+def measured_traffic(workload: str):
+    """HBM bytes per decode launch from the committed counter summary of this
+    workload, or None when it is absent or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"decode_kernel_{workload}_traffic.md")
     try:
-        with open(TRAFFIC_SUMMARY) as f:
+        with open(path) as f:
             text = f.read()
     except OSError:
         return None
@@ -95,7 +108,7 @@ def measured_traffic():
 
 
 class Ev:
-    """A pair of timing events on the current stream."""
+    """A pair of timing events, recorded on the current stream."""
 
     def __init__(self, torch):
         self.a = torch.cuda.Event(enable_timing=True)
@@ -105,11 +118,37 @@ class Ev:
         return self.a.elapsed_time(self.b)
 
 
+def timed(torch, fn, reps):
+    """Mean milliseconds of fn() over reps calls (one warm call first)."""
+    fn()
+    torch.cuda.synchronize()
+    e = Ev(torch)
+    e.a.record()
+    for _ in range(reps):
+        fn()
+    e.b.record()
+    torch.cuda.synchronize()
+    return e.ms() / reps
+
+
+def decode_graph(torch, steps, n):
+    """The n decode launches of `steps` captured into one HIP graph."""
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=cap):
+        for s_ in range(n):
+            steps.run(s_, stream=cap)
+    torch.cuda.synchronize()
+    return graph
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: there is no multi-GPU path (the kernels would shard by sequence or "
-              "kv head with no exchange). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: every GPU box here has one, and the library has no multi-GPU path "
+              "(prefill and decode would shard by sequence or kv head with no exchange). Run with --gpus 1.",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -124,38 +163,31 @@ def main():
     torch.cuda.set_device(0)
     uattn.lib()
 
-    w = inputs.qwen_gqa()
+    w = inputs.WORKLOADS[args.workload]()
     B, P, R = w.num_seqs, w.prompt_lens[0], w.response_lens[0]
     L = P + R
-    hq, hkv, d, page, V = w.num_q_heads, w.num_kv_heads, w.head_dim, w.page_size, w.vocab
+    hq, hkv, d, V = w.num_q_heads, w.num_kv_heads, w.head_dim, w.vocab
 
-    # ------------------------------------------------------------------ inputs
+    # ------------------------------------------------------------------ inputs (device, seeded)
     t0 = time.time()
-    host = inputs.packed_qkv(w)
-    cu = host["cu_seqlens"]
-
-    def to_dev(bits):
-        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
-
-    q, k, v = to_dev(host["q"]), to_dev(host["k"]), to_dev(host["v"])
-    cu_dev = torch.from_numpy(cu).to(dev)
-    table, npages = inputs.paged_layout(w.seq_lens, page)
-    kp = to_dev(inputs.scatter_to_pages(host["k"], cu, table, npages, page))
-    vp = to_dev(inputs.scatter_to_pages(host["v"], cu, table, npages, page))
-    table_dev = torch.from_numpy(table).to(dev)
-    # rollout prompt pack
-    pidx = torch.from_numpy(np.concatenate([np.arange(cu[b], cu[b] + P) for b in range(B)])).to(dev)
-    qp, kpk, vpk = q[pidx].contiguous(), k[pidx].contiguous(), v[pidx].contiguous()
-    cu_p = torch.from_numpy(inputs.cu_seqlens([P] * B)).to(dev)
-    # the rollout writes the prompt's K/V into the paged cache (same bits the cache already holds)
-    seq_p = torch.from_numpy(np.repeat(np.arange(B, dtype=np.int32), P)).to(dev)
-    pos_p = torch.from_numpy(np.tile(np.arange(P, dtype=np.int32), B)).to(dev)
-    # Q/K RMSNorm + NeoX RoPE over the full trajectories (its own buffers; the attention inputs stay raw)
+    pk = inputs.DevicePack(w, tag=205, build_pages=False)
+    cu = pk.cu
+    q_raw, k_raw, v = pk.q, pk.k, pk.v
+    cu_dev = pk.cu_dev
     pos_full = torch.from_numpy(np.concatenate([np.arange(n, dtype=np.int32) for n in w.seq_lens])).to(dev)
     qn_w = inputs.normal_bf16_device((d,), 1.0, 90, 0)
     kn_w = inputs.normal_bf16_device((d,), 1.0, 90, 1)
     cos_sin = uattn.rope_cache(L, d, 1e6)
-    q_rope, k_rope = torch.empty_like(q), torch.empty_like(k)
+    # attention inputs: the normalized, rotated q and k (the timed norm/RoPE phase rewrites the same bits)
+    q, k = uattn.qk_norm_rope(q_raw, k_raw, pos_full, qn_w, kn_w, cos_sin)
+    kp, vp = pk.pages(k, v)
+    table_dev = pk.table_dev
+    # rollout prompt pack
+    pidx = torch.from_numpy(np.concatenate([np.arange(cu[b], cu[b] + P) for b in range(B)])).to(dev)
+    qp, kpk, vpk = q[pidx].contiguous(), k[pidx].contiguous(), v[pidx].contiguous()
+    cu_p = torch.from_numpy(inputs.cu_seqlens([P] * B)).to(dev)
+    seq_p = torch.from_numpy(np.repeat(np.arange(B, dtype=np.int32), P)).to(dev)
+    pos_p = torch.from_numpy(np.tile(np.arange(P, dtype=np.int32), B)).to(dev)
     # decode steps: query of token P+s of every sequence; context P+s+1
     tok = torch.from_numpy((cu[:B][None, :] + P + np.arange(R)[:, None]).astype(np.int64)).to(dev)  # [R, B]
     q_steps = q[tok.reshape(-1)].reshape(R, B, hq, d).contiguous()
@@ -165,14 +197,14 @@ def main():
     out_prompt = torch.empty_like(qp)
     out_full = torch.empty_like(q)
     lse_full = torch.empty((q.shape[0], hq), dtype=torch.float32, device=dev)
+    q_rope, k_rope = torch.empty_like(q), torch.empty_like(k)
     # policy-update backward: upstream gradient ~ N(0,1), gradient buffers and workspace
     dout = inputs.normal_bf16_device(tuple(q.shape), 1.0, 7, 3)
     dq_b, dk_b, dv_b = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     bwd_ws = torch.empty(uattn.prefill_backward_workspace_bytes(q.shape[0], hq), dtype=torch.uint8, device=dev)
-    # log-prob leg: one row per response token
+    # LM head + log-prob of the response tokens: hidden states [rows, Hq*d] ~ N(0,1), weights ~ N(0, sigma^2/H),
+    # so the logits are ~ N(0, logit_sigma^2)
     rows = B * R
-    # LM head: hidden states [rows, Hq*d] ~ N(0,1) and weights ~ N(0, sigma^2/H), so the
-    # logits it produces are ~ N(0, logit_sigma^2); the log-prob leg reads them
     H = hq * d
     hidden = inputs.normal_bf16_device((rows, H), 1.0, 7, 1)
     lm_w = inputs.normal_bf16_device((V, H), w.logit_sigma / float(np.sqrt(H)), 7, 2)
@@ -180,7 +212,7 @@ def main():
     targets = torch.from_numpy(inputs.targets(rows, V)).to(dev)
     logp = torch.empty(rows, dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
-    log(f"inputs ready in {time.time() - t0:.1f}s: T={q.shape[0]} pages={npages} logits={tuple(logits.shape)}")
+    log(f"inputs ready in {time.time() - t0:.1f}s: {w.name} T={q.shape[0]} pages={pk.num_pages} logits={tuple(logits.shape)}")
     if args.calibration_copy:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         src.fill_(1)
@@ -191,19 +223,7 @@ def main():
         del src, dst
         log("calibration copy: 1 GiB device to device")
 
-    # ------------------------------------------------------------------ one step
-    # The 3072 token-wise decode launches run as one HIP graph (captured once,
-    # untimed), so the decode phase is not bound by host launch latency; every
-    # launch in it is a full uattn_decode call on the step's resident inputs.
-    graph = None
-    if not args.eager_decode:
-        cap = torch.cuda.Stream()
-        cap.wait_stream(torch.cuda.current_stream())
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=cap):
-            for s_ in range(R):
-                steps.run(s_, stream=cap)
-        torch.cuda.synchronize()
+    graph = None if args.eager_decode else decode_graph(torch, steps, R)
 
     def step(ev):
         ev["pre"].a.record()
@@ -220,13 +240,13 @@ def main():
                 steps.run(s_)
         ev["dec"].b.record()
         ev["nr"].a.record()
-        uattn.qk_norm_rope(q, k, pos_full, qn_w, kn_w, cos_sin, q_out=q_rope, k_out=k_rope)
+        uattn.qk_norm_rope(q_raw, k_raw, pos_full, qn_w, kn_w, cos_sin, q_out=q_rope, k_out=k_rope)
         ev["nr"].b.record()
         ev["upd"].a.record()
-        uattn.prefill(q, k, v, cu_dev, L, out=out_full, lse=lse_full)
+        uattn.prefill(q_rope, k_rope, v, cu_dev, L, out=out_full, lse=lse_full)
         ev["upd"].b.record()
         ev["bwd"].a.record()
-        uattn.prefill_backward(q, k, v, out_full, dout, lse_full, cu_dev, L, dq=dq_b, dk=dk_b, dv=dv_b,
+        uattn.prefill_backward(q_rope, k_rope, v, out_full, dout, lse_full, cu_dev, L, dq=dq_b, dk=dk_b, dv=dv_b,
                                workspace=bwd_ws)
         ev["bwd"].b.record()
         ev["lm"].a.record()
@@ -236,14 +256,11 @@ def main():
         uattn.logprob(logits, targets, out=logp)
         ev["lp"].b.record()
 
-    def new_events():
-        return {"pre": Ev(torch), "kvw": Ev(torch), "nr": Ev(torch), "upd": Ev(torch), "lm": Ev(torch),
-                "lp": Ev(torch), "dec": Ev(torch), "bwd": Ev(torch)}
-
-    for i in range(args.warmup):
-        step(new_events())
+    names = ("pre", "kvw", "dec", "nr", "upd", "bwd", "lm", "lp")
+    for _ in range(args.warmup):
+        step({n: Ev(torch) for n in names})
     torch.cuda.synchronize()
-    evs = [new_events() for _ in range(args.steps)]
+    evs = [{n: Ev(torch) for n in names} for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
@@ -254,71 +271,59 @@ def main():
 
     # ------------------------------------------------------------------ metrics
     K = args.steps
-    pre_ms = sum(e["pre"].ms() for e in evs) / K
-    upd_ms = sum(e["upd"].ms() for e in evs) / K
-    bwd_ms = sum(e["bwd"].ms() for e in evs) / K
-    lp_ms = sum(e["lp"].ms() for e in evs) / K
-    kvw_ms = sum(e["kvw"].ms() for e in evs) / K
-    nr_ms = sum(e["nr"].ms() for e in evs) / K
-    lm_ms = sum(e["lm"].ms() for e in evs) / K
-    dec_wall_ms = sum(e["dec"].ms() for e in evs) / K
-    dec_kernel_ms = dec_wall_ms
+    ph = {n: sum(e[n].ms() for e in evs) / K for n in names}
     step_ms = wall / K * 1e3
-
     upd_flop = w.prefill_flop()
     pre_flop = float(B * 2.0 * d * hq * P * (P + 1))
     dec_bytes = w.decode_kv_bytes()
     lp_bytes = float(rows) * V * 2
-    upd_tflops = upd_flop / (upd_ms * 1e-3) / 1e12
-    # backward: five products per causal (query, key) pair (S recomputed, dP, dV, dK, dQ) = 2.5 x forward
-    bwd_flop = 2.5 * upd_flop
-    bwd_tflops = bwd_flop / (bwd_ms * 1e-3) / 1e12
-    pre_tflops = pre_flop / (pre_ms * 1e-3) / 1e12
-    dec_gbs_wall = dec_bytes / (dec_wall_ms * 1e-3) / 1e9
-    lp_gbs = lp_bytes / (lp_ms * 1e-3) / 1e9
+    bwd_flop = 2.5 * upd_flop   # five products per causal (query, key) pair: S recomputed, dP, dV, dK, dQ
     kvw_bytes = float(B * P) * hkv * d * 2 * 2 * 2      # K and V rows read once and written once
-    kvw_gbs = kvw_bytes / (kvw_ms * 1e-3) / 1e9
     nr_bytes = float(q.numel() + k.numel()) * 2 * 2    # every q and k element read once and written once
-    nr_gbs = nr_bytes / (nr_ms * 1e-3) / 1e9
     lm_flop = 2.0 * rows * V * H
-    lm_tflops = lm_flop / (lm_ms * 1e-3) / 1e12
+    tf = lambda flop, ms: flop / (ms * 1e-3) / 1e12
+    gbs = lambda nbytes, ms: nbytes / (ms * 1e-3) / 1e9
+    dec_gbs = gbs(dec_bytes, ph["dec"])
+    upd_tflops = tf(upd_flop, ph["upd"])
 
     # ------------------------------------------------------------------ bitwise Eq. (1)
     full_bits = out_full.view(torch.int16)
-    dec_rows = out_steps.view(torch.int16).reshape(R * B, hq, d)
-    ref_rows = full_bits[tok.reshape(-1)]
-    dec_eq = (dec_rows == ref_rows).all(dim=-1)                 # [(R*B), hq]
+    dec_eq = (out_steps.view(torch.int16).reshape(R * B, hq, d) == full_bits[tok.reshape(-1)]).all(dim=-1)
+    n_dec, m_dec = dec_eq.numel(), int(dec_eq.sum().item())
     pr_eq = (out_prompt.view(torch.int16) == full_bits[pidx]).all(dim=-1)
-    n_rows = dec_eq.numel() + pr_eq.numel()
-    n_match = int(dec_eq.sum().item()) + int(pr_eq.sum().item())
-    bitwise_pct = 100.0 * n_match / n_rows
-    # unit reuse ratio of the decoded rows' log-probs is implied by bit equality of
-    # the rows; here also check the log-prob leg itself is batch invariant on a sample
-    sub = ua_rows = torch.arange(0, rows, max(1, rows // 64), device=dev)
+    n_pr, m_pr = pr_eq.numel(), int(pr_eq.sum().item())
+    rope_same = bool(torch.equal(q_rope.view(torch.int16), q.view(torch.int16))) and \
+        bool(torch.equal(k_rope.view(torch.int16), k.view(torch.int16)))
+    del dec_eq, pr_eq, full_bits
+    sub = torch.arange(0, rows, max(1, rows // 64), device=dev)
     lp_sub = uattn.logprob(logits[sub].contiguous(), targets[sub].contiguous())
     ratio_one = bool(torch.equal(lp_sub.view(torch.int32), logp[sub].view(torch.int32)))
-    del ua_rows
-    log(f"bitwise rows {n_match}/{n_rows}; logprob batch-invariant: {ratio_one}")
-    # the backward is deterministic: a second call into fresh buffers gives the same bits
-    grads2 = uattn.prefill_backward(q, k, v, out_full, dout, lse_full, cu_dev, L, workspace=bwd_ws)
+    log(f"bitwise: decode rows {m_dec}/{n_dec}, prompt rows {m_pr}/{n_pr}; norm/RoPE repeat equal {rope_same}; "
+        f"logprob batch-invariant {ratio_one}")
+    grads2 = uattn.prefill_backward(q_rope, k_rope, v, out_full, dout, lse_full, cu_dev, L, workspace=bwd_ws)
     bwd_repeat = all(bool(torch.equal(a.view(torch.int16), b.view(torch.int16)))
                      for a, b in zip((dq_b, dk_b, dv_b), grads2))
     del grads2
     log(f"backward repeat bitwise equal: {bwd_repeat}")
 
-    # ------------------------------------------------------------------ CPU oracle baseline
-    cpu = None
-    cpu_rows = None
+    # host copies for the CPU oracle (a bounded sample of the same decode work)
+    cpu_inputs = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, host, table, npages, args.cpu_seconds)
-        cpu_rows = cpu_row_baselines(w, host, table, npages, args.cpu_row_seconds)
+        cpu_inputs = {
+            "kp": inputs.host_bits(kp), "vp": inputs.host_bits(vp), "table": pk.table,
+            "q_steps": inputs.host_bits(q_steps), "P": P, "R": R, "B": B,
+        }
+    del pk, q_raw, k_raw, q, k, v, kp, vp, qp, kpk, vpk, q_steps, out_steps, out_prompt, out_full, lse_full
+    del q_rope, k_rope, dout, dq_b, dk_b, dv_b, bwd_ws, hidden, lm_w, logits, steps, graph
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
 
     dec_launch_bytes = dec_bytes / R
-    dec_launch_ms = dec_kernel_ms / R
-    traffic = measured_traffic()
+    dec_launch_ms = ph["dec"] / R
+    traffic = measured_traffic(w.name)
     result = {
         "metric": METRIC,
-        "value": round(dec_gbs_wall, 2),
+        "value": round(dec_gbs, 2),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": K,
@@ -330,184 +335,305 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "qwen_gqa: 8 seqs x (1024 prompt + 3072 response), 32 q / 8 kv heads, head_dim 128, "
-                        "bf16 N(0,0.25), page 64; logprob 24576 rows x vocab 151936, N(0,4)",
+            "workload": (f"{w.name}: {B} seqs x {L} tokens ({P} prompt + {R} decoded), {hq} q / {hkv} kv heads, "
+                         f"head_dim {d}, bf16 N(0,{w.sigma ** 2:g}), page {w.page_size}; logprob {rows} rows x vocab "
+                         f"{V}, N(0,{w.logit_sigma ** 2:g})"),
             "global_batch": B,
             "seq_len": L,
             "parallelism": "single GPU",
-            "value_is": "decode KV GB/s over the decode phase (3072 token-wise uattn_decode launches, batch 8, "
-                        "replayed as one HIP graph; HIP events around the phase)",
+            "value_is": (f"decode KV GB/s over the decode phase ({R} token-wise uattn_decode launches, batch {B}, "
+                         f"replayed as one HIP graph; HIP events around the phase)"),
         },
         "roofline": {
             "kernel": "decode_kernel (uattn_decode; split-KV with fused merge)",
             "bound": "hbm",
-            "achieved": round(dec_launch_bytes / (dec_launch_ms * 1e-3) / 1e9, 2),
+            "achieved": round(gbs(dec_launch_bytes, dec_launch_ms), 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(dec_launch_bytes / (dec_launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "frac": round(gbs(dec_launch_bytes, dec_launch_ms) / HBM_PEAK_GBS, 4),
             "traffic": traffic["hbm_bytes_per_launch"] if traffic else None,
             "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "traffic_over_algorithmic": round(traffic["hbm_bytes_per_launch"] / dec_launch_bytes, 4) if traffic else None,
             "bytes_per_launch": dec_launch_bytes,
             "avg_launch_ms": round(dec_launch_ms, 5),
-            "avg_launch_ms_is": "decode-phase event time / 3072 launches (includes the graph's inter-launch gaps)",
+            "avg_launch_ms_is": f"decode-phase event time / {R} launches (includes the graph's inter-launch gaps)",
         },
         "roofline_prefill": {
-            "kernel": "prefill_kernel (policy-update prefill over 8 x 4096)",
+            "kernel": f"prefill_kernel (policy-update prefill over {B} x {L})",
             "bound": "mfma",
             "achieved": round(upd_tflops, 2),
             "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(upd_tflops / BF16_PEAK_TFLOPS, 4),
             "flop_per_launch": upd_flop,
-            "avg_launch_ms": round(upd_ms, 4),
+            "avg_launch_ms": round(ph["upd"], 4),
         },
         "roofline_backward": {
-            "kernel": "uattn_prefill_backward (bwd_prep + bwd_dkdv + bwd_dq over 8 x 4096)",
+            "kernel": f"uattn_prefill_backward (bwd_prep + bwd_dkdv + bwd_dq over {B} x {L})",
             "bound": "mfma",
-            "achieved": round(bwd_tflops, 2),
+            "achieved": round(tf(bwd_flop, ph["bwd"]), 2),
             "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
-            "frac": round(bwd_tflops / BF16_PEAK_TFLOPS, 4),
+            "frac": round(tf(bwd_flop, ph["bwd"]) / BF16_PEAK_TFLOPS, 4),
             "flop_per_call": bwd_flop,
             "flop_is": "5 products x 2*d FLOP per causal (query, key) pair per q head (2.5 x the forward)",
-            "avg_call_ms": round(bwd_ms, 4),
+            "avg_call_ms": round(ph["bwd"], 4),
         },
-        "phases_ms": {"prompt_prefill": round(pre_ms, 4), "kv_write": round(kvw_ms, 4), "decode": round(dec_wall_ms, 3),
-                      "qk_norm_rope": round(nr_ms, 4), "lm_head": round(lm_ms, 4),
-                      "update_prefill": round(upd_ms, 4), "update_backward": round(bwd_ms, 4),
-                      "logprob": round(lp_ms, 4)},
-        "prompt_prefill_tflops": round(pre_tflops, 2),
-        "logprob_gbs": round(lp_gbs, 2),
-        "logprob_frac_hbm": round(lp_gbs / HBM_PEAK_GBS, 4),
-        "kv_write_gbs": round(kvw_gbs, 2),
-        "kv_write_frac_hbm": round(kvw_gbs / HBM_PEAK_GBS, 4),
-        "qk_norm_rope_gbs": round(nr_gbs, 2),
-        "qk_norm_rope_frac_hbm": round(nr_gbs / HBM_PEAK_GBS, 4),
-        "lm_head_tflops": round(lm_tflops, 2),
-        "lm_head_frac_mfma": round(lm_tflops / BF16_PEAK_TFLOPS, 4),
-        "bitwise_match_pct": round(bitwise_pct, 4),
-        "bitwise_rows": [n_match, n_rows],
+        "phases_ms": {"prompt_prefill": round(ph["pre"], 4), "kv_write": round(ph["kvw"], 4),
+                      "decode": round(ph["dec"], 3), "qk_norm_rope": round(ph["nr"], 4), "lm_head": round(ph["lm"], 4),
+                      "update_prefill": round(ph["upd"], 4), "update_backward": round(ph["bwd"], 4),
+                      "logprob": round(ph["lp"], 4)},
+        "prompt_prefill_tflops": round(tf(pre_flop, ph["pre"]), 2),
+        "logprob_gbs": round(gbs(lp_bytes, ph["lp"]), 2),
+        "logprob_frac_hbm": round(gbs(lp_bytes, ph["lp"]) / HBM_PEAK_GBS, 4),
+        "kv_write_gbs": round(gbs(kvw_bytes, ph["kvw"]), 2),
+        "kv_write_frac_hbm": round(gbs(kvw_bytes, ph["kvw"]) / HBM_PEAK_GBS, 4),
+        "qk_norm_rope_gbs": round(gbs(nr_bytes, ph["nr"]), 2),
+        "qk_norm_rope_frac_hbm": round(gbs(nr_bytes, ph["nr"]) / HBM_PEAK_GBS, 4),
+        "lm_head_tflops": round(tf(lm_flop, ph["lm"]), 2),
+        "lm_head_frac_mfma": round(tf(lm_flop, ph["lm"]) / BF16_PEAK_TFLOPS, 4),
+        "bitwise_match_pct": round(100.0 * m_dec / n_dec, 4),
+        "bitwise_match_is": "decoded (token, q head) rows bit-identical to the full-sequence prefill row",
+        "bitwise_decode_rows": [m_dec, n_dec],
+        "bitwise_prompt_rows": [m_pr, n_pr],
+        "bitwise_prompt_rows_are": "prompt-only rollout prefill rows vs the full-trajectory prefill at the same rows",
+        "norm_rope_repeat_bitwise": rope_same,
         "logprob_batch_invariant": ratio_one,
         "backward_repeat_bitwise": bwd_repeat,
-        "cpu_baseline": cpu,
-        "cpu_baselines_other_rows": cpu_rows,
     }
+
+    if not args.no_secondary:
+        result["secondary"] = secondary(torch, np, inputs, uattn)
+    if not args.no_ceilings:
+        result["measured_ceilings"] = ceilings(result)
+    if cpu_inputs is not None:
+        result["cpu_baseline"] = cpu_baseline(w, cpu_inputs, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(w, host, table, npages, budget_s):
-    """The fp64 oracle's token-wise decode on a bounded sample of the same
-    decode steps (one BLAS thread), in algorithmic KV GB/s."""
-    import numpy as np
-    from threadpoolctl import threadpool_limits
-
-    import oracle
-    from paper_2609_35140_amd import inputs
-
-    B, P, R = w.num_seqs, w.prompt_lens[0], w.response_lens[0]
-    cu = host["cu_seqlens"]
-    kp = inputs.scatter_to_pages(host["k"], cu, table, npages, w.page_size)
-    vp = inputs.scatter_to_pages(host["v"], cu, table, npages, w.page_size)
-    order = inputs.rng(11, 0).permutation(R)
-    done_bytes, done_steps = 0.0, 0
-    per_tok = 2 * w.num_kv_heads * w.head_dim * 2
-    with threadpool_limits(limits=1):
-        t0 = time.perf_counter()
-        for s in order:
-            n = P + int(s) + 1
-            qrows = host["q"][cu[:B] + n - 1]
-            oracle.paged_decode_fp64(qrows, kp, vp, table, [n] * B)
-            done_bytes += B * n * per_tok
-            done_steps += 1
-            if time.perf_counter() - t0 >= budget_s:
-                break
-        el = time.perf_counter() - t0
-    log(f"cpu oracle: {done_steps} decode steps in {el:.1f}s")
-    return {"value": round(done_bytes / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done_steps} of the 3072 decode steps (random order, batch 8, 32 q heads) through "
-                      f"oracle.paged_decode_fp64 in {el:.1f}s on 1 thread",
-            "seconds": round(el, 2)}
-
-
-def cpu_row_baselines(w, host, table, npages, budget_s):
-    """The fp64 oracle of every other row of the step on a bounded sample of the
-    same workload (one BLAS thread each), in the unit of that row's GPU figure.
-    Each row repeats its sample until `budget_s` seconds have passed."""
-    import numpy as np
-    from threadpoolctl import threadpool_limits
-
-    import oracle
-    from paper_2609_35140_amd import inputs
-
-    hq, hkv, d, P = w.num_q_heads, w.num_kv_heads, w.head_dim, w.prompt_lens[0]
-    grp = hq // hkv
-    cu = host["cu_seqlens"]
-
-    def timed(fn):
-        n, t0 = 0, time.perf_counter()
-        while True:
-            fn()
-            n += 1
-            el = time.perf_counter() - t0
-            if el >= budget_s:
-                return n, el
-
+def secondary(torch, np, inputs, uattn):
+    """Qwen-style GQA (decode phase and prefill), varlen-pack and GRPO-rollout
+    full-pack prefill throughput, with the Qwen-style decode rows checked bit
+    for bit against its prefill."""
     out = {}
-    with threadpool_limits(limits=1):
-        # prefill: the first 1024 positions of sequence 0, the 4 q heads of kv head 0
-        n = 1024
-        q = host["q"][:n, :grp]
-        k = host["k"][:n, :1]
-        v = host["v"][:n, :1]
-        flop = 4.0 * d * grp * n * (n + 1) / 2
-        reps, el = timed(lambda: oracle.causal_attention_fp64(q, k, v, [0, n]))
-        out["prefill"] = {"value": round(flop * reps / el / 1e12, 6), "unit": "TFLOP/s",
-                          "sample": f"oracle.causal_attention_fp64, 1 x {n} tokens x {grp} q heads, x{reps}"}
-        # backward: 512 positions, same heads, N(0,1) upstream gradient
-        n = 512
-        do = inputs.normal_bf16((n, grp, d), 1.0, 7, 3)
-        flop = 2.5 * 4.0 * d * grp * n * (n + 1) / 2
-        reps, el = timed(lambda: oracle.attention_backward_fp64(host["q"][:n, :grp], host["k"][:n, :1],
-                                                                 host["v"][:n, :1], do, [0, n]))
-        out["update_backward"] = {"value": round(flop * reps / el / 1e12, 6), "unit": "TFLOP/s",
-                                  "sample": f"oracle.attention_backward_fp64, 1 x {n} tokens x {grp} q heads, x{reps}"}
-        # LM head: 16 rows x a 8192-entry vocabulary slice x hidden Hq*d
-        H = hq * d
-        hid = inputs.normal_bf16((16, H), 1.0, 7, 4)
-        wt = inputs.normal_bf16((8192, H), w.logit_sigma / float(np.sqrt(H)), 7, 5)
-        reps, el = timed(lambda: oracle.logits_fp64(hid, wt))
-        out["lm_head"] = {"value": round(2.0 * 16 * 8192 * H * reps / el / 1e12, 6), "unit": "TFLOP/s",
-                          "sample": f"oracle.logits_fp64, 16 rows x 8192 vocab x {H}, x{reps}"}
-        # log-prob: 16 rows of the full vocabulary
-        lg = inputs.logits_bf16(16, w.vocab, w.logit_sigma, tag=9)
-        tg = inputs.targets(16, w.vocab, tag=9)
-        reps, el = timed(lambda: oracle.logprob_fp64(lg, tg))
-        out["logprob"] = {"value": round(16 * w.vocab * 2 * reps / el / 1e9, 4), "unit": "GB/s",
-                          "sample": f"oracle.logprob_fp64, 16 rows x {w.vocab}, x{reps}"}
-        # KV write: the prompt tokens of sequence 0 into a copy of the paged cache
-        kp = inputs.scatter_to_pages(host["k"], cu, table, npages, w.page_size)
-        vp = inputs.scatter_to_pages(host["v"], cu, table, npages, w.page_size)
-        kn, vn = host["k"][:P], host["v"][:P]
-        seq = np.zeros(P, dtype=np.int32)
-        pos = np.arange(P, dtype=np.int32)
-        reps, el = timed(lambda: oracle.kv_write(kp, vp, kn, vn, table, seq, pos))
-        out["kv_write"] = {"value": round(P * hkv * d * 2 * 2 * 2 * reps / el / 1e9, 4), "unit": "GB/s",
-                           "sample": f"oracle.kv_write, {P} tokens x {hkv} kv heads, x{reps}"}
-        # Q/K RMSNorm + NeoX RoPE: 256 tokens of sequence 0
-        n = 256
-        cs = oracle.rope_table(n, d, 1e6)
-        wq = inputs.normal_bf16((d,), 1.0, 90, 0)
-        wk = inputs.normal_bf16((d,), 1.0, 90, 1)
-        posn = np.arange(n)
-        reps, el = timed(lambda: (oracle.qk_norm_rope(host["q"][:n], posn, wq, 1e-6, cs),
-                                  oracle.qk_norm_rope(host["k"][:n], posn, wk, 1e-6, cs)))
-        out["qk_norm_rope"] = {"value": round(n * (hq + hkv) * d * 2 * 2 * reps / el / 1e9, 4), "unit": "GB/s",
-                               "sample": f"oracle.qk_norm_rope, {n} tokens x ({hq} + {hkv}) heads, x{reps}"}
-    for v in out.values():
-        v.update({"cores": 1, "kind": "oracle"})
-    log("cpu oracle rows: " + ", ".join(f"{k} {v['value']} {v['unit']}" for k, v in out.items()))
+    # Qwen-style GQA: 8 x (1024 + 3072), 32/8/128, page 64
+    w = inputs.qwen_gqa()
+    pk = inputs.DevicePack(w, tag=202)
+    B, P, R = w.num_seqs, w.prompt_lens[0], w.response_lens[0]
+    hq, d = w.num_q_heads, w.head_dim
+    L = P + R
+    tok = torch.from_numpy((pk.cu[:B][None, :] + P + np.arange(R)[:, None]).astype(np.int64)).cuda()
+    q_steps = pk.q[tok.reshape(-1)].reshape(R, B, hq, d).contiguous()
+    sl = torch.from_numpy(np.repeat((P + 1 + np.arange(R, dtype=np.int32))[:, None], B, axis=1)).cuda()
+    out_steps = torch.empty_like(q_steps)
+    steps = uattn.DecodeSteps(q_steps, pk.kp, pk.vp, pk.table_dev, sl, L, out_steps)
+    graph = decode_graph(torch, steps, R)
+    out_full = torch.empty_like(pk.q)
+    pre_ms = timed(torch, lambda: uattn.prefill(pk.q, pk.k, pk.v, pk.cu_dev, L, out=out_full), 5)
+    dec_ms = timed(torch, graph.replay, 5)
+    eq = (out_steps.view(torch.int16).reshape(R * B, hq, d) == out_full.view(torch.int16)[tok.reshape(-1)]).all(-1)
+    dec_bytes = w.decode_kv_bytes()
+    out["qwen_gqa"] = {
+        "workload": "8 seqs x (1024 prompt + 3072 decoded), 32 q / 8 kv heads, head_dim 128, bf16 N(0,0.25), page 64",
+        "decode_gbs": round(dec_bytes / (dec_ms * 1e-3) / 1e9, 2),
+        "decode_frac_hbm": round(dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "decode_launch_us": round(dec_ms / R * 1e3, 3),
+        "decode_kv_set_mb": round(B * L * w.num_kv_heads * d * 2 * 2 / 1e6, 1),
+        "decode_kv_set_note": "the whole KV cache fits the 256 MB Infinity Cache, so consecutive steps re-read cached pages",
+        "prefill_tflops": round(w.prefill_flop() / (pre_ms * 1e-3) / 1e12, 2),
+        "prefill_frac_mfma": round(w.prefill_flop() / (pre_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+        "prefill_ms": round(pre_ms, 4),
+        "bitwise_decode_rows": [int(eq.sum().item()), eq.numel()],
+    }
+    log(f"secondary qwen_gqa: {out['qwen_gqa']}")
+    del pk, q_steps, out_steps, steps, graph, out_full, eq
+    torch.cuda.empty_cache()
+    # full-pack prefill of the varlen training pack and of the GRPO rollout trajectories
+    for name, mk, tag in (("varlen_pack", inputs.varlen_pack, 203), ("grpo_rollout", inputs.grpo_rollout, 204)):
+        w = mk()
+        pk = inputs.DevicePack(w, tag=tag, build_pages=False)
+        o = torch.empty_like(pk.q)
+        ms = timed(torch, lambda: uattn.prefill(pk.q, pk.k, pk.v, pk.cu_dev, pk.max_seqlen, out=o), 3)
+        fl = w.prefill_flop()
+        out[f"{name}_prefill"] = {"tokens": w.total_tokens, "flop": fl, "ms": round(ms, 3),
+                                  "tflops": round(fl / (ms * 1e-3) / 1e12, 2),
+                                  "frac_mfma": round(fl / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)}
+        log(f"secondary {name} prefill: {out[f'{name}_prefill']}")
+        del pk, o
+        torch.cuda.empty_cache()
     return out
+
+
+def ceilings(result):
+    """Measured streaming-read and MFMA ceilings, and the headline fractions
+    against them (besides the datasheet peaks)."""
+    from paper_2609_35140_amd import ceilings as cl
+    seq = cl.read_gbs(4 << 30, paged=False)
+    paged = cl.read_gbs(4 << 30, block_bytes=16384, paged=True)
+    mfma = cl.mfma_tflops()
+    dec = result["roofline"]["achieved"]
+    pre = result["roofline_prefill"]["achieved"]
+    out = {"hbm_read_sequential_gbs": round(seq, 1), "hbm_read_paged_16kb_gbs": round(paged, 1),
+           "mfma_bf16_tflops": round(mfma, 1),
+           "decode_frac_of_paged_read": round(dec / paged, 4), "prefill_frac_of_measured_mfma": round(pre / mfma, 4),
+           "method": "4 GiB buffer read once per launch (16-byte loads, 4 in flight per lane, XOR-folded), "
+                     "contiguous or as 16 KB blocks in a random permutation; 8 independent "
+                     "v_mfma_f32_16x16x32_bf16 chains per wave, 8 waves per CU, no memory traffic"}
+    log(f"measured ceilings: {out}")
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        txt = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in txt.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def run_pool(tasks, fn, threads, budget_s):
+    """Run fn(task) over `tasks` on `threads` threads until the tasks or the
+    time budget run out (a started task always finishes).  Returns the list
+    of completed results and the elapsed seconds."""
+    lock = threading.Lock()
+    it = iter(tasks)
+    done = []
+    t0 = time.perf_counter()
+
+    def worker():
+        while True:
+            if time.perf_counter() - t0 >= budget_s:
+                return
+            with lock:
+                task = next(it, None)
+            if task is None:
+                return
+            r = fn(task)
+            with lock:
+                done.append(r)
+
+    ths = [threading.Thread(target=worker) for _ in range(threads)]
+    for t in ths:
+        t.start()
+    for t in ths:
+        t.join()
+    return done, time.perf_counter() - t0
+
+
+def cpu_baseline(w, ci, budget_s):
+    """The CPU oracle on the host's cores, on bounded samples of the headline
+    decode work: the fp64 definition (paged decode, one task per (step,
+    entry)) and the fp32 tile-order emulator (one task per (entry, q head,
+    8 steps)), each on all cores (one thread per core, one BLAS thread each).
+    Rates are in work units of (row, key) pairs; seconds are extrapolated to
+    every configuration's full prefill and decode sets by that ratio, and the
+    tiny configuration is also run in full."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    from paper_2609_35140_amd import inputs
+
+    threads = len(os.sched_getaffinity(0))
+    hq, hkv, d = w.num_q_heads, w.num_kv_heads, w.head_dim
+    grp = hq // hkv
+    P, R, B = ci["P"], ci["R"], ci["B"]
+    kp, vp, table, qs = ci["kp"], ci["vp"], ci["table"], ci["q_steps"]
+    per_tok = 2 * hkv * d * 2
+    g = inputs.rng(11, 0)
+    scale = oracle.default_scale(d)
+
+    # fp64 definition: decode entries of random steps
+    tasks64 = [(int(s), b) for s in g.permutation(R) for b in range(B)]
+
+    def f64(task):
+        s, b = task
+        n = P + s + 1
+        oracle.paged_decode_fp64(qs[s, b:b + 1], kp, vp, table[b:b + 1], [n])
+        return n
+
+    with threadpool_limits(limits=1):
+        done, el64 = run_pool(tasks64, f64, threads, budget_s)
+    ctx64 = float(sum(done))
+    gbs = ctx64 * per_tok / el64 / 1e9
+    rate64 = ctx64 * hq / el64            # (row, key) pairs per second
+    log(f"cpu oracle fp64: {len(done)} decode entries in {el64:.1f}s on {threads} threads ({gbs:.3f} GB/s)")
+
+    # fp32 emulator: rows of one (entry, head) over 8 random steps at a time
+    def keys_of(b, kvh, n):
+        return oracle.gather_paged(kp, table[b], n, kvh), oracle.gather_paged(vp, table[b], n, kvh)
+
+    steps8 = g.permutation(R)
+    tasks32 = [(b, h, steps8[i:i + 8]) for i in range(0, R, 8) for b in range(B) for h in g.permutation(hq)[:4]]
+
+    def f32(task):
+        b, h, ss = task
+        n = P + int(max(ss)) + 1
+        kk, vv = keys_of(b, h // grp, n)
+        oracle.tile_emulate_rows_fp32(qs[ss, b, h], kk, vv, [P + int(s) for s in ss], scale)
+        return float(sum(P + int(s) + 1 for s in ss))
+
+    with threadpool_limits(limits=1):
+        done32, el32 = run_pool(tasks32, f32, threads, budget_s)
+    rate32 = float(sum(done32)) / el32
+    log(f"cpu emulator fp32: {len(done32)} tasks ({8 * len(done32)} rows) in {el32:.1f}s on {threads} threads")
+
+    # work of every configuration's full sets, in (row, key) pairs
+    def pairs(wl, decode_rows=None):
+        pre = wl.num_q_heads * sum(L * (L + 1) / 2 for L in wl.seq_lens)
+        if decode_rows is None:
+            dec = wl.num_q_heads * sum(sum(range(p + 1, p + r + 1)) for p, r in zip(wl.prompt_lens, wl.response_lens))
+        else:
+            dec = decode_rows
+        return pre, dec
+
+    extrap = {}
+    for name in ("tiny", "qwen_gqa", "varlen_pack", "grpo_rollout", "long_context"):
+        wl = inputs.WORKLOADS[name]()
+        if name == "varlen_pack":  # prefill only; its decode set is 4096 random tokens (mean context ~ L/2)
+            pre, _ = pairs(wl)
+            dec = wl.num_q_heads * 4096 * float(np.mean(wl.seq_lens)) / 2
+        else:
+            pre, dec = pairs(wl)
+        extrap[name] = {"prefill_pairs": pre, "decode_pairs": dec,
+                        "fp64_s": {"prefill": round(pre / rate64, 1), "decode": round(dec / rate64, 1)},
+                        "fp32_emulator_s": {"prefill": round(pre / rate32, 1), "decode": round(dec / rate32, 1)}}
+    # the tiny configuration in full, both oracles
+    tw = inputs.tiny()
+    t = inputs.packed_qkv(tw, seed=42)
+    with threadpool_limits(limits=threads):
+        a = time.perf_counter()
+        oracle.causal_attention_fp64(t["q"], t["k"], t["v"], t["cu_seqlens"])
+        tiny64 = time.perf_counter() - a
+        a = time.perf_counter()
+        oracle.tile_emulate_fp32(t["q"], t["k"], t["v"], t["cu_seqlens"])
+        tiny32 = time.perf_counter() - a
+    extrap["tiny"]["measured_full_s"] = {"fp64": round(tiny64, 3), "fp32_emulator": round(tiny32, 3)}
+    return {
+        "value": round(gbs, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+        "cpu_model": cpu_model(),
+        "sample": (f"{len(done)} decode entries (random steps of the {R}-step, batch-{B} decode, {hq} q heads, "
+                   f"contexts {P + 1}..{P + R}) through oracle.paged_decode_fp64 in {el64:.1f}s, one task per thread "
+                   f"on {threads} threads"),
+        "seconds": round(el64, 2),
+        "fp64_pairs_per_s": round(rate64, 1),
+        "fp32_emulator": {"rows": 8 * len(done32), "seconds": round(el32, 2), "pairs_per_s": round(rate32, 1),
+                          "sample": "rows of one (entry, q head) at 8 random decode steps per task, "
+                                    "oracle.tile_emulate_rows_fp32 on the paged context"},
+        "extrapolated": extrap,
+        "extrapolation_is": "seconds = full-set (row, key) pairs / the sample's pairs per second; prefill sets "
+                            "are every causal pair of the pack, decode sets every decoded row's context",
+    }
 
 
 if __name__ == "__main__":

@@ -10,6 +10,9 @@ the HIP kernels or the binding, and neither imports the other.
 from .attention import (  # noqa: F401
     CHUNK_KEYS,
     LSE_ABS,
+    MAX_ABS,
+    MEAN_ABS,
+    REL_BF16,
     TILE_KEYS,
     attention_row_fp64,
     attention_rows_fp64,
@@ -21,6 +24,7 @@ from .attention import (  # noqa: F401
     parity_report,
     round_to_bf16,
     tile_emulate_fp32,
+    tile_emulate_rows_fp32,
     to_bf16_bits,
 )
 from .kv_cache import kv_write  # noqa: F401

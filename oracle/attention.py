@@ -317,6 +317,21 @@ def tile_emulate_fp32(q: np.ndarray, k: np.ndarray, v: np.ndarray, cu_seqlens: S
     return o, lse
 
 
+def tile_emulate_rows_fp32(qrows: np.ndarray, keys: np.ndarray, vals: np.ndarray, qpos: Sequence[int],
+                           scale: float, bn: int = TILE_KEYS, chunk: int = CHUNK_KEYS) -> Tuple[np.ndarray, np.ndarray]:
+    """The fp32 tile-order emulation for rows of ONE head against an explicit
+    context (the emulator's counterpart of ``attention_row_fp64``).
+
+    qrows [R,d] (bf16 bits or float), keys/vals [n,d] with n > max(qpos):
+    row r attends keys 0..qpos[r].  Returns (o [R,d] float32 holding bf16
+    values, lse [R] float32), exactly what ``tile_emulate_fp32`` gives for
+    the same rows.
+    """
+    qpos = np.asarray(qpos, dtype=np.int64)
+    c = np.float32(np.float64(np.float32(scale)) * LOG2E)
+    return _emulate_rows(_as_f64(qrows), _as_f64(keys), _as_f64(vals), qpos, c, bn, chunk)
+
+
 # --------------------------------------------------------------------------
 # the parity gate
 # --------------------------------------------------------------------------

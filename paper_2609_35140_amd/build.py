@@ -25,6 +25,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libuattn.so")
+# measured-ceiling microbenchmarks (streaming read, MFMA), a library of their own
+CEIL_SRC = os.path.join(PKG, "ceilings", "uattn_ceilings.hip")
+CEIL_LIB = os.path.join(PKG, "libuattn_ceilings.so")
 
 ARCH = "gfx950"
 COMMON_FLAGS = [
@@ -73,10 +76,17 @@ def _compile(src: str, defines, resource_usage: bool):
 
 
 def build(resource_usage: bool = False, out: str = LIB, verbose: bool = False, defines=()) -> str:
-    """Compile every source to its own object (in parallel), then link the library."""
+    """Compile every source to its own object (in parallel), then link the
+    library; then the measured-ceiling library."""
+    _build_lib(sources(), out, resource_usage, verbose, defines)
+    if out == LIB:
+        _build_lib([CEIL_SRC], CEIL_LIB, False, verbose, ())
+    return out
+
+
+def _build_lib(srcs, out, resource_usage, verbose, defines):
     from concurrent.futures import ThreadPoolExecutor
     os.makedirs(OBJDIR, exist_ok=True)
-    srcs = sources()
     with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         results = list(ex.map(lambda f: _compile(f, defines, resource_usage), srcs))
     for obj, cmd, res in results:

@@ -111,11 +111,14 @@ size_t uattn_decode_workspace_bytes(int32_t batch, int32_t max_seqlen, int32_t n
          uattn::decode_ws_ml_bytes(batch, nchunk, num_q_heads);
 }
 
-uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
-                          const int32_t* seqlens, int32_t batch, int32_t max_pages_per_seq, int32_t page_size,
-                          int32_t num_pages, int32_t max_seqlen, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                          float softmax_scale, void* out, float* lse, void* workspace, size_t workspace_bytes,
-                          void* stream) {
+}  // extern "C"
+
+namespace uattn {
+uattn_status decode_prepare(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+                            const int32_t* seqlens, int32_t batch, int32_t max_pages_per_seq, int32_t page_size,
+                            int32_t num_pages, int32_t max_seqlen, int32_t num_q_heads, int32_t num_kv_heads,
+                            int32_t head_dim, float softmax_scale, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, DecodeLaunch* launch) {
   if (batch < 0 || max_pages_per_seq < 0 || max_seqlen < 0 || num_pages < 0 || num_q_heads <= 0 ||
       num_kv_heads <= 0)
     return UATTN_EINVAL;
@@ -124,7 +127,10 @@ uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_page
   if (page_size < 16 || (page_size & (page_size - 1)) != 0) return UATTN_EUNSUPPORTED;
   if (num_q_heads / num_kv_heads > uattn::kMaxGroup) return UATTN_EUNSUPPORTED;
   if (batch > 65535 || num_kv_heads > 65535) return UATTN_EUNSUPPORTED;
-  if (batch == 0) return UATTN_OK;
+  if (batch == 0) {
+    launch->batch = 0;
+    return UATTN_OK;
+  }
   if (max_seqlen == 0 || num_pages == 0) return UATTN_EINVAL;  // every entry holds at least its own token
   if (static_cast<int64_t>(max_pages_per_seq) * page_size < max_seqlen) return UATTN_EINVAL;
   if (!q || !k_pages || !v_pages || !block_table || !seqlens || !out) return UATTN_EINVAL;
@@ -145,7 +151,7 @@ uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_page
           return UATTN_EINVAL;
     }
   }
-  uattn::DecodeLaunch a;
+  DecodeLaunch a;
   a.q = q;
   a.k_pages = k_pages;
   a.v_pages = v_pages;
@@ -180,6 +186,24 @@ uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_page
   a.head_dim = head_dim;
   a.num_cus = uattn::device_cus();
   a.c = exp2_scale(softmax_scale);
+  *launch = a;
+  return UATTN_OK;
+}
+}  // namespace uattn
+
+extern "C" {
+
+uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+                          const int32_t* seqlens, int32_t batch, int32_t max_pages_per_seq, int32_t page_size,
+                          int32_t num_pages, int32_t max_seqlen, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                          float softmax_scale, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  uattn::DecodeLaunch a;
+  const uattn_status st =
+      uattn::decode_prepare(q, k_pages, v_pages, block_table, seqlens, batch, max_pages_per_seq, page_size, num_pages,
+                            max_seqlen, num_q_heads, num_kv_heads, head_dim, softmax_scale, out, lse, workspace,
+                            workspace_bytes, &a);
+  if (st != UATTN_OK || a.batch == 0) return st;
   return uattn::launch_decode(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
 }
 

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/uattn.h"
+
 namespace uattn {
 
 struct PrefillLaunch {
@@ -126,6 +128,16 @@ int32_t device_cus();
 hipError_t launch_prefill(const PrefillLaunch& a, hipStream_t stream);
 hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream);
 hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t stream);
+
+// Checks uattn_decode's arguments (every rule of uattn.h) and fills the launch
+// record, laying the workspace out as counters at its start and partials at
+// its end.  Returns the status uattn_decode reports; `launch->batch` is 0
+// when there is nothing to launch.
+uattn_status decode_prepare(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+                            const int32_t* seqlens, int32_t batch, int32_t max_pages_per_seq, int32_t page_size,
+                            int32_t num_pages, int32_t max_seqlen, int32_t num_q_heads, int32_t num_kv_heads,
+                            int32_t head_dim, float softmax_scale, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, DecodeLaunch* launch);
 
 // Decode workspace: arrival counters at the start (kept zero between calls),
 // the fp32 partials (acc, then m/l) at the end of the caller's buffer.

@@ -269,3 +269,129 @@ def normal_bf16_device(shape, sigma: float, *key: int, seed: int = BASE_SEED, de
         flat[lo:hi] = (tmp * sigma).to(torch.bfloat16)
         del tmp
     return out
+
+
+NAN_BF16 = 0x7FC0
+
+
+def host_bits(t) -> np.ndarray:
+    """bf16 device tensor -> its bits on the host (numpy uint16)."""
+    import torch
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+class DevicePack:
+    """A packed varlen batch drawn on the GPU, plus its paged KV cache.
+
+    With ``w.shared_prompt_group > 1`` the sequences of a group carry the same
+    prompt tokens, and (``share_prompt_pages``) the group's full prompt pages
+    are stored once and referenced by every member's block table, as a
+    serving engine's prefix cache would.
+    """
+
+    def __init__(self, w, tag: int, seed: int = BASE_SEED, share_prompt_pages: bool = True, extra_pages: int = 7,
+                 build_pages: bool = True):
+        import torch
+        self.w = w
+        hq, hkv, d = w.num_q_heads, w.num_kv_heads, w.head_dim
+        lens = [int(x) for x in w.seq_lens]
+        P = [int(x) for x in w.prompt_lens]
+        self.cu = cu_seqlens(lens)
+        cu = self.cu
+        T = int(cu[-1])
+        self.max_seqlen = max(lens)
+        sig = w.sigma
+        G = int(w.shared_prompt_group)
+        if G > 1:
+            self.q = torch.empty((T, hq, d), dtype=torch.bfloat16, device="cuda")
+            self.k = torch.empty((T, hkv, d), dtype=torch.bfloat16, device="cuda")
+            self.v = torch.empty((T, hkv, d), dtype=torch.bfloat16, device="cuda")
+            for grp in range(w.num_seqs // G):
+                p0 = P[grp * G]
+                pq = normal_bf16_device((p0, hq, d), sig, tag, 1, grp, 0, seed=seed)
+                pk = normal_bf16_device((p0, hkv, d), sig, tag, 1, grp, 1, seed=seed)
+                pv = normal_bf16_device((p0, hkv, d), sig, tag, 1, grp, 2, seed=seed)
+                for s in range(grp * G, grp * G + G):
+                    lo = int(cu[s])
+                    self.q[lo:lo + p0] = pq
+                    self.k[lo:lo + p0] = pk
+                    self.v[lo:lo + p0] = pv
+            for s in range(w.num_seqs):
+                lo, hi = int(cu[s]) + P[s], int(cu[s + 1])
+                if hi > lo:
+                    self.q[lo:hi] = normal_bf16_device((hi - lo, hq, d), sig, tag, 2, s, 0, seed=seed)
+                    self.k[lo:hi] = normal_bf16_device((hi - lo, hkv, d), sig, tag, 2, s, 1, seed=seed)
+                    self.v[lo:hi] = normal_bf16_device((hi - lo, hkv, d), sig, tag, 2, s, 2, seed=seed)
+        else:
+            self.q = normal_bf16_device((T, hq, d), sig, tag, 0, 0, seed=seed)
+            self.k = normal_bf16_device((T, hkv, d), sig, tag, 0, 1, seed=seed)
+            self.v = normal_bf16_device((T, hkv, d), sig, tag, 0, 2, seed=seed)
+        self.cu_dev = torch.from_numpy(cu).cuda()
+
+        # ---- block table over a shuffled pool of physical pages
+        page = int(w.page_size)
+        self.page = page
+        npg = [(L + page - 1) // page for L in lens]
+        shared = share_prompt_pages and G > 1
+        n_pp = [P[s] // page if shared else 0 for s in range(w.num_seqs)]  # shared full prompt pages
+        n_group_pages = sum(n_pp[g * G] for g in range(w.num_seqs // G)) if shared else 0
+        own = [npg[s] - n_pp[s] for s in range(w.num_seqs)]
+        total = n_group_pages + sum(own) + extra_pages
+        perm = rng(9, tag, seed=seed).permutation(total).astype(np.int32)
+        maxp = max(npg)
+        table = np.full((w.num_seqs, maxp), -1, dtype=np.int32)
+        pos = 0
+        if shared:
+            for grp in range(w.num_seqs // G):
+                n = n_pp[grp * G]
+                pages = perm[pos:pos + n]
+                pos += n
+                for s in range(grp * G, grp * G + G):
+                    table[s, :n] = pages
+        for s in range(w.num_seqs):
+            table[s, n_pp[s]:npg[s]] = perm[pos:pos + own[s]]
+            pos += own[s]
+        self.table = table
+        self.num_pages = total
+        self.table_dev = torch.from_numpy(table).cuda()
+
+        self.kp = self.vp = None
+        if build_pages:
+            self.kp, self.vp = self.pages(self.k, self.v)
+
+    def pages(self, k, v):
+        """Paged copies [num_pages, Hkv, page, d] of packed k, v [T, Hkv, d]:
+        token t of sequence b at position j goes to page table[b, j // page],
+        slot j % page; slots no token maps to hold a bf16 NaN."""
+        import torch
+        w, page, T = self.w, self.page, int(self.cu[-1])
+        lens = [int(x) for x in w.seq_lens]
+        seq_of = np.repeat(np.arange(w.num_seqs, dtype=np.int64), lens)
+        posn = np.arange(T, dtype=np.int64) - self.cu[:-1].astype(np.int64)[seq_of]
+        pg = torch.from_numpy(self.table[seq_of, posn // page].astype(np.int64)).cuda()
+        sl = torch.from_numpy(posn % page).cuda()
+        nan = torch.tensor(NAN_BF16, dtype=torch.int16).view(torch.bfloat16).item()
+        shape = (self.num_pages, w.num_kv_heads, page, w.head_dim)
+        kp = torch.full(shape, nan, dtype=torch.bfloat16, device="cuda")
+        vp = torch.full(shape, nan, dtype=torch.bfloat16, device="cuda")
+        kp[pg, :, sl, :] = k
+        vp[pg, :, sl, :] = v
+        return kp, vp
+
+    def decode_rows(self, entries):
+        """Decode inputs for (sequence, position) entries: the query of token
+        `position` of `sequence`, context position + 1, the sequence's block
+        table row.  Returns (q, table, seqlens, max_seqlen, packed token ids)."""
+        import torch
+        seqs = np.array([s for s, _ in entries], dtype=np.int64)
+        pos = np.array([p for _, p in entries], dtype=np.int64)
+        tok = self.cu[seqs].astype(np.int64) + pos
+        q = self.q[torch.from_numpy(tok).cuda()].contiguous()
+        table = torch.from_numpy(np.ascontiguousarray(self.table[seqs])).cuda()
+        seqlens = torch.from_numpy((pos + 1).astype(np.int32)).cuda()
+        return q, table, seqlens, int(pos.max()) + 1, tok
+
+    def host_sequence(self, s: int):
+        """Q, K, V bits of sequence s (for oracle rows)."""
+        lo, hi = int(self.cu[s]), int(self.cu[s + 1])
+        return host_bits(self.q[lo:hi]), host_bits(self.k[lo:hi]), host_bits(self.v[lo:hi])

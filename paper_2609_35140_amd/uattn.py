@@ -193,9 +193,17 @@ def decode_workspace_bytes(batch: int, max_seqlen: int, num_q_heads: int, head_d
 
 
 def new_workspace(nbytes: int, device="cuda"):
-    """A zero-filled decode workspace (the counters it holds must start at zero)."""
+    """A zero-filled decode workspace (the counters it holds must start at zero).
+
+    The returned tensor carries the extent of its known-zero prefix as an
+    attribute of the tensor object itself, so the binding never re-zeroes it
+    needlessly and never trusts a stale record: a different tensor (even one
+    at the same device address) starts with no such record.
+    """
     import torch
-    return torch.zeros(int(nbytes), dtype=torch.uint8, device=device)
+    t = torch.zeros(int(nbytes), dtype=torch.uint8, device=device)
+    t._uattn_zero_prefix = int(nbytes)
+    return t
 
 
 def counter_bytes(batch: int, num_q_heads: int) -> int:
@@ -203,18 +211,34 @@ def counter_bytes(batch: int, num_q_heads: int) -> int:
     return (4 * batch * num_q_heads + 255) // 256 * 256
 
 
-# counter-region size of the last call on each caller-provided workspace
-_ws_counter_extent = {}
+def _partials_start(ws_bytes: int, batch: int, max_seqlen: int, num_q_heads: int, head_dim: int) -> int:
+    """Byte offset where a call's fp32 partials begin (they sit at the end of
+    the workspace; the counters at its start)."""
+    nchunk = (max_seqlen + CHUNK_KEYS - 1) // CHUNK_KEYS
+    acc = (4 * batch * num_q_heads * nchunk * head_dim + 255) // 256 * 256
+    ml = (4 * batch * num_q_heads * nchunk * 2 + 255) // 256 * 256
+    return (ws_bytes & ~15) - acc - ml
 
 
-def _prepare_workspace(workspace, batch: int, num_q_heads: int):
-    """Zero the counter region of a caller-provided workspace when the uattn.h
-    rule requires it: first use here, or a larger region than the last call."""
-    key = workspace.data_ptr()
-    c = min(counter_bytes(batch, num_q_heads), workspace.numel() * workspace.element_size())
-    if _ws_counter_extent.get(key, -1) < c:
-        workspace.view(-1).view(dtype=workspace.dtype)[: c // workspace.element_size()].zero_()
-    _ws_counter_extent[key] = c
+def _prepare_workspace(workspace, batch: int, max_seqlen: int, num_q_heads: int, head_dim: int):
+    """Make the counter region of ``workspace`` zero before a call, as uattn.h
+    requires, and record what the call leaves zero.
+
+    The record lives on the tensor object (``_uattn_zero_prefix``), never in
+    a table keyed by address: a workspace tensor this binding has not seen
+    before (or a different view of the same memory) is zeroed on first use,
+    whatever an earlier tensor at that address held.  After the call the
+    counters are zero again (the kernel resets them), while the partial
+    region at the end of the buffer holds data.
+    """
+    nbytes = workspace.numel() * workspace.element_size()
+    c = min(counter_bytes(batch, num_q_heads), nbytes)
+    known = getattr(workspace, "_uattn_zero_prefix", 0)
+    if known < c:
+        workspace.view(-1)[: c // workspace.element_size()].zero_()
+        known = c
+    workspace._uattn_zero_prefix = max(c, min(known, _partials_start(nbytes, batch, max_seqlen, num_q_heads,
+                                                                        head_dim)))
 
 
 def decode(q, k_pages, v_pages, block_table, seqlens, max_seqlen: int, softmax_scale: Optional[float] = None,
@@ -248,9 +272,9 @@ def decode(q, k_pages, v_pages, block_table, seqlens, max_seqlen: int, softmax_s
     need = decode_workspace_bytes(B, int(max_seqlen), hq, d) if B > 0 else 0
     if workspace is None and need > 0:
         workspace = new_workspace(need, q.device)
-        _ws_counter_extent[workspace.data_ptr()] = counter_bytes(B, hq)
-    elif workspace is not None and need > 0:
-        _prepare_workspace(workspace, B, hq)
+    if workspace is not None and need > 0:
+        _need(workspace.is_cuda and workspace.is_contiguous(), "workspace must be a contiguous GPU tensor")
+        _prepare_workspace(workspace, B, int(max_seqlen), hq, d)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_load().uattn_decode(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table), _ptr(seqlens), B,
                                 block_table.shape[1], page, k_pages.shape[0], int(max_seqlen), hq, hkv, d, float(softmax_scale),
@@ -399,8 +423,9 @@ class DecodeSteps:
         need = decode_workspace_bytes(B, int(max_seqlen), hq, d)
         if workspace is None and need > 0:
             workspace = new_workspace(need, q_steps.device)
-        elif workspace is not None and need > 0:
-            _prepare_workspace(workspace, B, hq)
+        if workspace is not None and need > 0:
+            _need(workspace.is_cuda and workspace.is_contiguous(), "workspace must be a contiguous GPU tensor")
+            _prepare_workspace(workspace, B, int(max_seqlen), hq, d)
         self.workspace = workspace
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         st = _stream(stream)

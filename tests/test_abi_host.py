@@ -191,3 +191,22 @@ def test_backward_argument_checks(lib, kw, code):
     assert lib.uattn_prefill_backward(a["q"], a["k"], a["v"], a["out"], a["dout"], a["lse"], a["cu"], a["ns"], a["T"],
                                       a["maxs"], a["hq"], a["hkv"], a["d"], a["scale"], a["dq"], a["dk"], a["dv"],
                                       a["ws"], a["wsb"], a["stream"]) == code
+
+
+def test_ceilings_library_exports_its_header():
+    from paper_2609_35140_amd import build, ceilings
+    if not os.path.exists(ceilings.LIB_PATH):
+        build.build()
+    src = open(os.path.join(ROOT, "include", "uattn_ceilings.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = sorted(set(re.findall(r"\b(uattn_[a-z_0-9]+)\s*\(", src)))
+    assert names == ["uattn_ceiling_mfma", "uattn_ceiling_read", "uattn_ceiling_read_grid"]
+    so = ctypes.CDLL(ceilings.LIB_PATH)
+    for n in names:
+        getattr(so, n)
+    lib = ceilings.lib()
+    # argument checks before any GPU call
+    assert lib.uattn_ceiling_read(P(16), None, 4, 4096, P(16), None) == 1      # block not a multiple of 16 KB
+    assert lib.uattn_ceiling_read(P(18), None, 4, 16384, P(16), None) == 1     # misaligned
+    assert lib.uattn_ceiling_read(P(16), None, 0, 16384, P(16), None) == 0     # nothing to read
+    assert lib.uattn_ceiling_mfma(0, 10, P(16), None) == 1

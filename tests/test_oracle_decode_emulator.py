@@ -160,3 +160,20 @@ def test_emulator_rising_scores_move_the_reference_within_gate():
     assert rep["pass"], rep
     assert np.max(np.abs(lse32 - lse64)) < oracle.LSE_ABS
 
+
+
+def test_emulator_one_head_rows_equal_pack_rows():
+    # the per-head entry (explicit context) gives the same bits as the pack entry
+    w = inputs.custom(4, 2, 64, [700, 300], sigma=1.0)
+    t = inputs.packed_qkv(w, seed=5)
+    cu = t["cu_seqlens"]
+    rows = [(cu[0] + 699, 3), (cu[0] + 256, 3), (cu[0] + 5, 3), (cu[1] + 299, 1)]
+    o_ref, l_ref = oracle.tile_emulate_fp32(t["q"], t["k"], t["v"], cu, rows=rows)
+    scale = oracle.default_scale(64)
+    for i, (tok, h) in enumerate(rows):
+        b = 0 if tok < cu[1] else 1
+        lo = int(cu[b])
+        o, l = oracle.tile_emulate_rows_fp32(t["q"][tok:tok + 1, h], t["k"][lo:cu[b + 1], h // 2],
+                                             t["v"][lo:cu[b + 1], h // 2], [tok - lo], scale)
+        assert np.array_equal(o[0].view(np.uint32), o_ref[i].view(np.uint32))
+        assert np.float32(l[0]).view(np.uint32) == np.float32(l_ref[i]).view(np.uint32)
