@@ -49,7 +49,8 @@ typedef enum {
   UATTN_EINVAL = 1,       /* null pointer, negative or inconsistent sizes, Hq % Hkv != 0, bad scale */
   UATTN_EUNSUPPORTED = 2, /* head_dim not 64/128, page_size not a power of two >= 16, group > 32 */
   UATTN_EWORKSPACE = 3,   /* decode workspace missing or smaller than uattn_decode_workspace_bytes() */
-  UATTN_ELAUNCH = 4       /* the HIP runtime rejected a kernel launch */
+  UATTN_ELAUNCH = 4,      /* the HIP runtime rejected a kernel launch */
+  UATTN_ESCRATCH = 5      /* uattn_decode_noalloc: the sizes need more than UATTN_DECODE_SCRATCH_BYTES */
 } uattn_status;
 
 /* Version of this ABI (UATTN_ABI_VERSION). */
@@ -139,6 +140,39 @@ uattn_status uattn_decode(const void* q, const void* k_pages, const void* v_page
                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                           float softmax_scale, void* out, float* lse,
                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * uattn_decode for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops or harnesses that forbid hipMalloc).
+ *
+ * Arguments, results and errors are those of uattn_decode, without the
+ * workspace: the fp32 partials and arrival counters live in a static device
+ * array of UATTN_DECODE_SCRATCH_BYTES bytes that the library owns, one per
+ * GPU, held until the process ends.  The call allocates and frees nothing:
+ * on the first call on a device it looks up that device's array
+ * (hipGetSymbolAddress); every call then zeroes the array's counter region
+ * with a small kernel and launches the decode kernel on `stream`, so the
+ * call may be captured into a HIP graph.  Results are bit-identical to
+ * uattn_decode's.
+ *
+ * Sizes whose uattn_decode_workspace_bytes(batch, max_seqlen, num_q_heads,
+ * head_dim) exceeds UATTN_DECODE_SCRATCH_BYTES return UATTN_ESCRATCH before
+ * any HIP call (e.g. 64 MiB holds batch 8 x 64 q heads x 32K keys, or batch
+ * 64 x 32 q heads x 16K keys).  Every call on a GPU shares that GPU's array
+ * and leaves its contents behind: calls that overlap on one GPU (streams
+ * not ordered with respect to each other) race and give wrong results; order
+ * them on one stream.
+ */
+#define UATTN_DECODE_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* UATTN_DECODE_SCRATCH_BYTES, as built into the library. */
+size_t uattn_decode_scratch_limit(void);
+
+uattn_status uattn_decode_noalloc(const void* q, const void* k_pages, const void* v_pages,
+                                  const int32_t* block_table, const int32_t* seqlens, int32_t batch,
+                                  int32_t max_pages_per_seq, int32_t page_size, int32_t num_pages, int32_t max_seqlen,
+                                  int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                  float softmax_scale, void* out, float* lse, void* stream);
 
 /*
  * Per-token log-probability of the recorded token (Section 3.1: the same

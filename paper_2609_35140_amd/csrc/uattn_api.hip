@@ -61,6 +61,7 @@ const char* uattn_status_string(int32_t status) {
     case UATTN_EUNSUPPORTED: return "UATTN_EUNSUPPORTED: unsupported shape";
     case UATTN_EWORKSPACE: return "UATTN_EWORKSPACE: workspace missing or too small";
     case UATTN_ELAUNCH: return "UATTN_ELAUNCH: kernel launch failed";
+    case UATTN_ESCRATCH: return "UATTN_ESCRATCH: these sizes need more decode scratch than the library's static array holds";
     default: return "UATTN_UNKNOWN_STATUS";
   }
 }

@@ -45,6 +45,11 @@ def _load():
     lib.uattn_decode.restype = c_i32
     lib.uattn_decode.argtypes = [c_p, c_p, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_f,
                                  c_p, c_p, c_p, c_sz, c_p]
+    lib.uattn_decode_scratch_limit.restype = c_sz
+    lib.uattn_decode_scratch_limit.argtypes = []
+    lib.uattn_decode_noalloc.restype = c_i32
+    lib.uattn_decode_noalloc.argtypes = [c_p, c_p, c_p, c_p, c_p, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                         c_i32, c_f, c_p, c_p, c_p]
     lib.uattn_logprob.restype = c_i32
     lib.uattn_logprob.argtypes = [c_p, c_i64, c_p, c_i32, c_i32, c_f, c_p, c_p]
     lib.uattn_qk_norm_rope.restype = c_i32
@@ -279,6 +284,44 @@ def decode(q, k_pages, v_pages, block_table, seqlens, max_seqlen: int, softmax_s
     _check(_load().uattn_decode(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table), _ptr(seqlens), B,
                                 block_table.shape[1], page, k_pages.shape[0], int(max_seqlen), hq, hkv, d, float(softmax_scale),
                                 _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream)))
+    return (out, lse) if lse is not None else out
+
+
+def decode_scratch_limit() -> int:
+    """Bytes of the library's static decode scratch array (uattn_decode_noalloc)."""
+    return int(_load().uattn_decode_scratch_limit())
+
+
+def decode_noalloc(q, k_pages, v_pages, block_table, seqlens, max_seqlen: int, softmax_scale: Optional[float] = None,
+                   out=None, return_lse: bool = False, lse=None, stream=None):
+    """uattn_decode_noalloc: the token-wise decode with the library's static
+    scratch array as its workspace (the call itself allocates nothing; pass
+    ``out``/``lse`` to keep this binding from allocating them).  Arguments and
+    results as for :func:`decode`."""
+    import torch
+    for name, t in (("q", q), ("k_pages", k_pages), ("v_pages", v_pages)):
+        _bf16_cuda(t, name)
+    _need(q.dim() == 3 and k_pages.dim() == 4 and v_pages.shape == k_pages.shape, "shapes: q [B,Hq,d], pages [P,Hkv,page,d]")
+    B, hq, d = q.shape
+    _, hkv, page, d2 = k_pages.shape
+    _need(d2 == d, "head_dim mismatch")
+    for name, t in (("block_table", block_table), ("seqlens", seqlens)):
+        _need(t.dtype == torch.int32 and t.is_cuda and t.is_contiguous(), f"{name} must be contiguous int32 on the GPU")
+    _need(block_table.dim() == 2 and block_table.shape[0] == B and seqlens.shape == (B,), "block_table/seqlens shape")
+    if softmax_scale is None:
+        softmax_scale = default_scale(d)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _bf16_cuda(out, "out")
+        _need(out.shape == q.shape, "out shape")
+    if return_lse and lse is None:
+        lse = torch.empty((B, hq), dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse.dtype == torch.float32 and lse.is_contiguous() and tuple(lse.shape) == (B, hq), "lse must be [B,Hq] fp32")
+    _check(_load().uattn_decode_noalloc(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table), _ptr(seqlens), B,
+                                        block_table.shape[1], page, k_pages.shape[0], int(max_seqlen), hq, hkv, d,
+                                        float(softmax_scale), _ptr(out), _ptr(lse), _stream(stream)))
     return (out, lse) if lse is not None else out
 
 

@@ -45,7 +45,7 @@ def test_abi_version_and_status_strings(lib):
     from paper_2609_35140_amd import uattn
     assert uattn.abi_version() == 1
     assert uattn.status_string(0) == "UATTN_OK"
-    for code in range(1, 5):
+    for code in range(1, 6):
         assert uattn.status_string(code).startswith("UATTN_E")
     assert "UNKNOWN" in uattn.status_string(99)
 
@@ -191,6 +191,36 @@ def test_backward_argument_checks(lib, kw, code):
     assert lib.uattn_prefill_backward(a["q"], a["k"], a["v"], a["out"], a["dout"], a["lse"], a["cu"], a["ns"], a["T"],
                                       a["maxs"], a["hq"], a["hkv"], a["d"], a["scale"], a["dq"], a["dk"], a["dv"],
                                       a["ws"], a["wsb"], a["stream"]) == code
+
+
+def test_decode_noalloc_limits(lib):
+    from paper_2609_35140_amd import uattn
+    assert uattn.decode_scratch_limit() == 64 << 20
+    # sizes the static scratch holds: the Qwen-style and long-context decode batches
+    assert uattn.decode_workspace_bytes(8, 4096, 32, 128) <= uattn.decode_scratch_limit()
+    assert uattn.decode_workspace_bytes(8, 32768, 64, 128) <= uattn.decode_scratch_limit()
+    # ... and one it does not: 512 sequences of 16K keys
+    assert uattn.decode_workspace_bytes(512, 16384, 32, 128) > uattn.decode_scratch_limit()
+
+
+def _decode_noalloc(lib, **kw):
+    a = dict(q=P(16), kp=P(16), vp=P(16), bt=P(16), sl=P(16), B=2, maxp=4, page=16, npages=10, maxs=64, hq=8, hkv=2,
+             d=128, scale=0.1, out=P(32), lse=None, stream=None)
+    a.update(kw)
+    return lib.uattn_decode_noalloc(a["q"], a["kp"], a["vp"], a["bt"], a["sl"], a["B"], a["maxp"], a["page"],
+                                    a["npages"], a["maxs"], a["hq"], a["hkv"], a["d"], a["scale"], a["out"], a["lse"],
+                                    a["stream"])
+
+
+# single-chunk sizes (no scratch needed, so no HIP call before the checks) and
+# sizes beyond the static array (refused by host arithmetic alone)
+@pytest.mark.parametrize("kw,code", [
+    (dict(hq=9), 1), (dict(page=24), 2), (dict(d=80), 2), (dict(maxp=3), 1), (dict(maxs=0), 1), (dict(bt=None), 1),
+    (dict(scale=0.0), 1), (dict(B=0), 0),
+    (dict(B=512, maxs=16384, maxp=1024, hq=32, hkv=8), 5), (dict(B=64, maxs=65536, maxp=4096, hq=64, hkv=8), 5),
+])
+def test_decode_noalloc_argument_checks(lib, kw, code):
+    assert _decode_noalloc(lib, **kw) == code
 
 
 def test_ceilings_library_exports_its_header():
