@@ -15,7 +15,8 @@ One step = one pass of the whole path over that batch:
      policy-update prefill over them (full-sequence entry point) and its
      backward
   4. the batch-invariant LM head (hidden 8192 -> 151,936 logits) of the
-     8 x 1024 response tokens, and their log-probabilities
+     8 x 1024 response tokens fused with their log-probabilities, and the
+     stand-alone log-probability over the same (stored) logits
 
 Attention everywhere runs on the normalized, rotated Q/K (the rotated K is
 what the paged cache holds and the decode queries are the rotated rows), so
@@ -211,6 +212,9 @@ def main():
     logits = torch.empty((rows, V), dtype=torch.bfloat16, device=dev)
     targets = torch.from_numpy(inputs.targets(rows, V)).to(dev)
     logp = torch.empty(rows, dtype=torch.float32, device=dev)
+    logp_fused = torch.empty(rows, dtype=torch.float32, device=dev)
+    lmlp_ws = torch.empty(uattn.lm_head_logprob_workspace_bytes(rows, V), dtype=torch.uint8, device=dev)
+    uattn.lm_head(hidden, lm_w, out=logits)  # the logits the stand-alone log-prob phase reads
     torch.cuda.synchronize()
     log(f"inputs ready in {time.time() - t0:.1f}s: {w.name} T={q.shape[0]} pages={pk.num_pages} logits={tuple(logits.shape)}")
     if args.calibration_copy:
@@ -250,7 +254,7 @@ def main():
                                workspace=bwd_ws)
         ev["bwd"].b.record()
         ev["lm"].a.record()
-        uattn.lm_head(hidden, lm_w, out=logits)
+        uattn.lm_head_logprob(hidden, lm_w, targets, out=logp_fused, workspace=lmlp_ws)
         ev["lm"].b.record()
         ev["lp"].a.record()
         uattn.logprob(logits, targets, out=logp)
@@ -298,8 +302,12 @@ def main():
     sub = torch.arange(0, rows, max(1, rows // 64), device=dev)
     lp_sub = uattn.logprob(logits[sub].contiguous(), targets[sub].contiguous())
     ratio_one = bool(torch.equal(lp_sub.view(torch.int32), logp[sub].view(torch.int32)))
+    lpf_sub = uattn.lm_head_logprob(hidden[sub].contiguous(), lm_w, targets[sub].contiguous())
+    fused_ratio_one = bool(torch.equal(lpf_sub.view(torch.int32), logp_fused[sub].view(torch.int32)))
+    fused_vs_two_call = float((logp_fused.double() - logp.double()).abs().max().item())
+    lm_alone_ms = timed(torch, lambda: uattn.lm_head(hidden, lm_w, out=logits), 2)
     log(f"bitwise: decode rows {m_dec}/{n_dec}, prompt rows {m_pr}/{n_pr}; norm/RoPE repeat equal {rope_same}; "
-        f"logprob batch-invariant {ratio_one}")
+        f"logprob batch-invariant {ratio_one}, fused {fused_ratio_one}; fused vs two-call max |d| {fused_vs_two_call:.3g}")
     grads2 = uattn.prefill_backward(q_rope, k_rope, v, out_full, dout, lse_full, cu_dev, L, workspace=bwd_ws)
     bwd_repeat = all(bool(torch.equal(a.view(torch.int16), b.view(torch.int16)))
                      for a, b in zip((dq_b, dk_b, dv_b), grads2))
@@ -314,7 +322,7 @@ def main():
             "q_steps": inputs.host_bits(q_steps), "P": P, "R": R, "B": B,
         }
     del pk, q_raw, k_raw, q, k, v, kp, vp, qp, kpk, vpk, q_steps, out_steps, out_prompt, out_full, lse_full
-    del q_rope, k_rope, dout, dq_b, dk_b, dv_b, bwd_ws, hidden, lm_w, logits, steps, graph
+    del q_rope, k_rope, dout, dq_b, dk_b, dv_b, bwd_ws, hidden, lm_w, logits, steps, graph, lmlp_ws
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
 
@@ -380,7 +388,8 @@ def main():
             "avg_call_ms": round(ph["bwd"], 4),
         },
         "phases_ms": {"prompt_prefill": round(ph["pre"], 4), "kv_write": round(ph["kvw"], 4),
-                      "decode": round(ph["dec"], 3), "qk_norm_rope": round(ph["nr"], 4), "lm_head": round(ph["lm"], 4),
+                      "decode": round(ph["dec"], 3), "qk_norm_rope": round(ph["nr"], 4),
+                      "lm_head_logprob_fused": round(ph["lm"], 4),
                       "update_prefill": round(ph["upd"], 4), "update_backward": round(ph["bwd"], 4),
                       "logprob": round(ph["lp"], 4)},
         "prompt_prefill_tflops": round(tf(pre_flop, ph["pre"]), 2),
@@ -390,8 +399,12 @@ def main():
         "kv_write_frac_hbm": round(gbs(kvw_bytes, ph["kvw"]) / HBM_PEAK_GBS, 4),
         "qk_norm_rope_gbs": round(gbs(nr_bytes, ph["nr"]), 2),
         "qk_norm_rope_frac_hbm": round(gbs(nr_bytes, ph["nr"]) / HBM_PEAK_GBS, 4),
-        "lm_head_tflops": round(tf(lm_flop, ph["lm"]), 2),
-        "lm_head_frac_mfma": round(tf(lm_flop, ph["lm"]) / BF16_PEAK_TFLOPS, 4),
+        "lm_head_logprob_fused_tflops": round(tf(lm_flop, ph["lm"]), 2),
+        "lm_head_logprob_fused_frac_mfma": round(tf(lm_flop, ph["lm"]) / BF16_PEAK_TFLOPS, 4),
+        "lm_head_alone_ms": round(lm_alone_ms, 4),
+        "lm_head_alone_plus_logprob_ms": round(lm_alone_ms + ph["lp"], 4),
+        "fused_logprob_batch_invariant": fused_ratio_one,
+        "fused_vs_two_call_logprob_max_abs": fused_vs_two_call,
         "bitwise_match_pct": round(100.0 * m_dec / n_dec, 4),
         "bitwise_match_is": "decoded (token, q head) rows bit-identical to the full-sequence prefill row",
         "bitwise_decode_rows": [m_dec, n_dec],
@@ -468,8 +481,8 @@ def ceilings(result):
     """Measured streaming-read and MFMA ceilings, and the headline fractions
     against them (besides the datasheet peaks)."""
     from paper_2609_35140_amd import ceilings as cl
-    seq = cl.read_gbs(4 << 30, paged=False)
-    paged = cl.read_gbs(4 << 30, block_bytes=16384, paged=True)
+    seq = max(cl.read_gbs(4 << 30, paged=False, nontemporal=nt) for nt in (False, True))
+    paged = max(cl.read_gbs(4 << 30, block_bytes=16384, paged=True, nontemporal=nt) for nt in (False, True))
     mfma = cl.mfma_tflops()
     dec = result["roofline"]["achieved"]
     pre = result["roofline_prefill"]["achieved"]
@@ -477,7 +490,8 @@ def ceilings(result):
            "mfma_bf16_tflops": round(mfma, 1),
            "decode_frac_of_paged_read": round(dec / paged, 4), "prefill_frac_of_measured_mfma": round(pre / mfma, 4),
            "method": "4 GiB buffer read once per launch (16-byte loads, 4 in flight per lane, XOR-folded), "
-                     "contiguous or as 16 KB blocks in a random permutation; 8 independent "
+                     "contiguous or as 16 KB blocks in a random permutation, the faster of plain and non-temporal "
+                     "loads; 8 independent "
                      "v_mfma_f32_16x16x32_bf16 chains per wave, 8 waves per CU, no memory traffic"}
     log(f"measured ceilings: {out}")
     return out

@@ -287,6 +287,47 @@ uattn_status uattn_lm_head(const void* hidden, int64_t hidden_stride, const void
                            void* stream);
 
 /*
+ * Bytes of device workspace uattn_lm_head_logprob needs for these sizes:
+ * two fp32 partials per (row, 256-entry vocabulary tile) and one per row.
+ * Pure host arithmetic; 0 for invalid sizes.
+ */
+size_t uattn_lm_head_logprob_workspace_bytes(int32_t num_rows, int32_t vocab);
+
+/*
+ * The LM head fused with the per-token log-probability (Section 3.1: the
+ * token log-probability after one deterministic logit processing, with the
+ * logits themselves batch-invariant):
+ *
+ *   z[t][v]  = bf16( sum_k hidden[t][k] * weight[v][k] )     (exactly uattn_lm_head's logits)
+ *   logp[t]  = x[t][targets[t]] - log sum_v exp(x[t][v]),   x = z * inv_temperature
+ *
+ * computed without a round trip of the logits through memory: the GEMM's
+ * epilogue reduces each row's logits of every 256-entry vocabulary tile to a
+ * (max, sum of exp) pair in a fixed order (lanes, then the tile's four waves)
+ * and picks out the target's logit; a second kernel folds each row's pairs in
+ * ascending tile order.  The order depends only on vocabulary positions, so
+ * a row's logp is bit-identical whatever num_rows or its place in the batch
+ * (the reuse ratio of the two regimes is exactly 1).  It is not bit-identical
+ * to uattn_logprob over the same logits, whose reduction is ordered
+ * differently (both are within rounding of the exact value).
+ *
+ *   hidden, weight, num_rows, vocab, hidden_dim, strides: as uattn_lm_head
+ *   targets    [num_rows] int32; a target outside [0, vocab) gives NaN
+ *   inv_temperature  finite, > 0
+ *   logp       [num_rows] fp32 (written)
+ *   logits     [num_rows, logits_stride] bf16, or NULL: when given, the
+ *              logits are stored as well (the same bits as uattn_lm_head)
+ *   workspace  device scratch of at least
+ *              uattn_lm_head_logprob_workspace_bytes(num_rows, vocab) bytes,
+ *              4-byte aligned, no initial contents needed; calls sharing a
+ *              workspace must be ordered on one stream
+ */
+uattn_status uattn_lm_head_logprob(const void* hidden, int64_t hidden_stride, const void* weight,
+                                   int64_t weight_stride, const int32_t* targets, int32_t num_rows, int32_t vocab,
+                                   int32_t hidden_dim, float inv_temperature, float* logp, void* logits,
+                                   int64_t logits_stride, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Bytes of device workspace uattn_prefill_backward needs: two fp32 values
  * per (token, q head).  Pure host arithmetic; 0 for invalid sizes.
  */

@@ -36,13 +36,14 @@ extern "C" {
  *                src + block_table[i] * block_bytes), or NULL for the
  *                identity order (one contiguous stream); entries are trusted
  *   block_bytes  a multiple of 16384
+ *   flags        0, or 1 for loads with the non-temporal cache hint
  *   checksum     [grid] uint32 (written), grid = uattn_ceiling_read_grid()
  *
  * The XOR of all `grid` checksum words equals the XOR of every 32-bit word of
  * the blocks read, whatever the order.
  */
 int32_t uattn_ceiling_read(const void* src, const int32_t* block_table, int64_t num_blocks, int64_t block_bytes,
-                           uint32_t* checksum, void* stream);
+                           int32_t flags, uint32_t* checksum, void* stream);
 
 /* Workgroups uattn_ceiling_read launches on the current device. */
 int32_t uattn_ceiling_read_grid(void);

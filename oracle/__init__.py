@@ -28,7 +28,7 @@ from .attention import (  # noqa: F401
     to_bf16_bits,
 )
 from .kv_cache import kv_write  # noqa: F401
-from .lm_head import abs_dot, logits_bf16, logits_fp64  # noqa: F401
+from .lm_head import abs_dot, lm_head_logprob_fp64, logits_bf16, logits_fp64  # noqa: F401
 from .logprob import logprob_fp64  # noqa: F401
 from .norm_rope import qk_norm_rope, rms_norm_bf16, rope_neox, rope_table  # noqa: F401
 from .attention_backward import attention_backward_fp64, backward_error_scales, dq_rows_fp64  # noqa: F401

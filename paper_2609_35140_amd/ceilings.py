@@ -21,7 +21,7 @@ def _load():
         lib = ctypes.CDLL(LIB_PATH)
         c_i32, c_i64, c_p = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
         lib.uattn_ceiling_read.restype = c_i32
-        lib.uattn_ceiling_read.argtypes = [c_p, c_p, c_i64, c_i64, c_p, c_p]
+        lib.uattn_ceiling_read.argtypes = [c_p, c_p, c_i64, c_i64, c_i32, c_p, c_p]
         lib.uattn_ceiling_read_grid.restype = c_i32
         lib.uattn_ceiling_read_grid.argtypes = []
         lib.uattn_ceiling_mfma.restype = c_i32
@@ -47,7 +47,7 @@ def _time(fn, reps):
     return a.elapsed_time(b) / reps
 
 
-def read(src, block_table=None, block_bytes: int = 16384, checksum=None):
+def read(src, block_table=None, block_bytes: int = 16384, checksum=None, nontemporal: bool = False):
     """Launch one streaming read of `src` (a uint8/any CUDA tensor) in blocks of
     `block_bytes`, in the order of `block_table` (int32 CUDA, or None for the
     identity order).  Returns the checksum tensor [grid] uint32 (as int32)."""
@@ -58,13 +58,15 @@ def read(src, block_table=None, block_bytes: int = 16384, checksum=None):
     if checksum is None:
         checksum = torch.empty(lib.uattn_ceiling_read_grid(), dtype=torch.int32, device=src.device)
     code = lib.uattn_ceiling_read(src.data_ptr(), None if block_table is None else block_table.data_ptr(), nblocks,
-                                  block_bytes, checksum.data_ptr(), torch.cuda.current_stream().cuda_stream)
+                                  block_bytes, 1 if nontemporal else 0, checksum.data_ptr(),
+                                  torch.cuda.current_stream().cuda_stream)
     if code != 0:
         raise RuntimeError(f"uattn_ceiling_read failed with code {code}")
     return checksum
 
 
-def read_gbs(nbytes: int = 4 << 30, block_bytes: int = 16384, paged: bool = False, reps: int = 10, seed: int = 0):
+def read_gbs(nbytes: int = 4 << 30, block_bytes: int = 16384, paged: bool = False, reps: int = 10, seed: int = 0,
+             nontemporal: bool = False):
     """Measured streaming-read GB/s over a buffer of `nbytes` (well above the
     256 MB Infinity Cache), contiguous or in a random block order."""
     import torch
@@ -76,7 +78,7 @@ def read_gbs(nbytes: int = 4 << 30, block_bytes: int = 16384, paged: bool = Fals
         g.manual_seed(seed)
         table = torch.randperm(nbytes // block_bytes, generator=g, device="cuda").to(torch.int32)
     ck = torch.empty(_load().uattn_ceiling_read_grid(), dtype=torch.int32, device="cuda")
-    ms = _time(lambda: read(src, table, block_bytes, ck), reps)
+    ms = _time(lambda: read(src, table, block_bytes, ck, nontemporal), reps)
     del src, table
     torch.cuda.empty_cache()
     return nbytes / (ms * 1e-3) / 1e9

@@ -23,6 +23,8 @@ int read_grid() {
 
 // Workgroup w reads blocks w, w + grid, ...; a block is read as consecutive
 // 4 KB rounds (256 lanes x 16 bytes), kUnroll rounds issued before use.
+// NT: the loads carry the non-temporal hint.
+template <bool NT>
 __global__ __launch_bounds__(kThreads) void read_kernel(const u32x4* __restrict__ src,
                                                        const int32_t* __restrict__ table, int64_t nblocks,
                                                        int64_t pieces_per_block, uint32_t* __restrict__ checksum) {
@@ -34,7 +36,12 @@ __global__ __launch_bounds__(kThreads) void read_kernel(const u32x4* __restrict_
     for (int64_t r = 0; r < pieces_per_block; r += kThreads * kUnroll) {
       u32x4 v[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) v[u] = p[r + u * kThreads];
+      for (int u = 0; u < kUnroll; ++u) {
+        if constexpr (NT)
+          v[u] = __builtin_nontemporal_load(p + r + u * kThreads);
+        else
+          v[u] = p[r + u * kThreads];
+      }
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) acc ^= v[u];
     }
@@ -48,6 +55,9 @@ __global__ __launch_bounds__(kThreads) void read_kernel(const u32x4* __restrict_
   if (tid == 0) checksum[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
 }
 
+// The eight accumulators are named registers of one inline-assembly block,
+// so the compiler can neither merge nor rotate them: eight independent
+// dependency chains per wave, each MFMA reading its own previous result.
 __global__ __launch_bounds__(kThreads) void mfma_kernel(int32_t waves, int32_t iters, float* __restrict__ out) {
   const int lane = threadIdx.x & 63;
   const int wave = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
@@ -57,16 +67,24 @@ __global__ __launch_bounds__(kThreads) void mfma_kernel(int32_t waves, int32_t i
     a[e] = static_cast<__bf16>(static_cast<float>((lane + e) & 7) * 0.125f);
     b[e] = static_cast<__bf16>(static_cast<float>((lane * 3 + e) & 7) * 0.0625f);
   }
-  f32x4 c[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) c[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0, c4 = c0, c5 = c0, c6 = c0, c7 = c0;
   for (int it = 0; it < iters; ++it) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) c[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c[i], 0, 0, 0);
+    asm volatile(
+        "v_mfma_f32_16x16x32_bf16 %0, %8, %9, %0\n\t"
+        "v_mfma_f32_16x16x32_bf16 %1, %8, %9, %1\n\t"
+        "v_mfma_f32_16x16x32_bf16 %2, %8, %9, %2\n\t"
+        "v_mfma_f32_16x16x32_bf16 %3, %8, %9, %3\n\t"
+        "v_mfma_f32_16x16x32_bf16 %4, %8, %9, %4\n\t"
+        "v_mfma_f32_16x16x32_bf16 %5, %8, %9, %5\n\t"
+        "v_mfma_f32_16x16x32_bf16 %6, %8, %9, %6\n\t"
+        "v_mfma_f32_16x16x32_bf16 %7, %8, %9, %7"
+        : "+v"(c0), "+v"(c1), "+v"(c2), "+v"(c3), "+v"(c4), "+v"(c5), "+v"(c6), "+v"(c7)
+        : "v"(a), "v"(b));
   }
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) s += c[i][0] + c[i][1] + c[i][2] + c[i][3];
+  // wait states before vector instructions read the last results
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+  const f32x4 c = ((c0 + c1) + (c2 + c3)) + ((c4 + c5) + (c6 + c7));
+  const float s = (c[0] + c[1]) + (c[2] + c[3]);
   if (lane == 0 && wave < waves) out[wave] = s;
 }
 
@@ -77,12 +95,16 @@ extern "C" {
 int32_t uattn_ceiling_read_grid(void) { return read_grid(); }
 
 int32_t uattn_ceiling_read(const void* src, const int32_t* block_table, int64_t num_blocks, int64_t block_bytes,
-                           uint32_t* checksum, void* stream) {
-  if (num_blocks < 0 || block_bytes <= 0 || (block_bytes % (kThreads * kUnroll * 16)) != 0) return 1;
+                           int32_t flags, uint32_t* checksum, void* stream) {
+  if (num_blocks < 0 || block_bytes <= 0 || (flags & ~1) != 0 || (block_bytes % (kThreads * kUnroll * 16)) != 0) return 1;
   if (num_blocks == 0) return 0;
   if (src == nullptr || checksum == nullptr || (reinterpret_cast<uintptr_t>(src) & 15u) != 0) return 1;
-  hipLaunchKernelGGL(read_kernel, dim3(read_grid()), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
-                     static_cast<const u32x4*>(src), block_table, num_blocks, block_bytes / 16, checksum);
+  if (flags & 1)
+    hipLaunchKernelGGL(read_kernel<true>, dim3(read_grid()), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
+                       static_cast<const u32x4*>(src), block_table, num_blocks, block_bytes / 16, checksum);
+  else
+    hipLaunchKernelGGL(read_kernel<false>, dim3(read_grid()), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
+                       static_cast<const u32x4*>(src), block_table, num_blocks, block_bytes / 16, checksum);
   return hipGetLastError() == hipSuccess ? 0 : 4;
 }
 

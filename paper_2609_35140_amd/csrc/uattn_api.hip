@@ -337,6 +337,50 @@ uattn_status uattn_lm_head(const void* hidden, int64_t hidden_stride, const void
   return uattn::launch_lm_head(a, static_cast<hipStream_t>(stream)) == hipSuccess ? UATTN_OK : UATTN_ELAUNCH;
 }
 
+size_t uattn_lm_head_logprob_workspace_bytes(int32_t num_rows, int32_t vocab) {
+  if (num_rows <= 0 || vocab <= 0) return 0;
+  return uattn::lm_head_logprob_ws_bytes(num_rows, vocab);
+}
+
+uattn_status uattn_lm_head_logprob(const void* hidden, int64_t hidden_stride, const void* weight,
+                                   int64_t weight_stride, const int32_t* targets, int32_t num_rows, int32_t vocab,
+                                   int32_t hidden_dim, float inv_temperature, float* logp, void* logits,
+                                   int64_t logits_stride, void* workspace, size_t workspace_bytes, void* stream) {
+  if (num_rows < 0 || vocab < 0 || hidden_dim <= 0 || (hidden_dim % 64) != 0) return UATTN_EINVAL;
+  if (hidden_stride < hidden_dim || weight_stride < hidden_dim) return UATTN_EINVAL;
+  if ((hidden_stride % 8) != 0 || (weight_stride % 8) != 0) return UATTN_EINVAL;
+  if (logits != nullptr && (logits_stride < vocab || (logits_stride % 8) != 0 || !aligned16(logits)))
+    return UATTN_EINVAL;
+  if (!scale_ok(inv_temperature)) return UATTN_EINVAL;
+  if (num_rows == 0) return UATTN_OK;
+  if (vocab == 0) return UATTN_EINVAL;  // log-softmax over an empty vocabulary
+  if (!hidden || !weight || !targets || !logp) return UATTN_EINVAL;
+  if (!aligned16(hidden) || !aligned16(weight)) return UATTN_EINVAL;
+  const size_t need = uattn_lm_head_logprob_workspace_bytes(num_rows, vocab);
+  if (workspace == nullptr || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 3u) != 0)
+    return UATTN_EWORKSPACE;
+  if (validate_env()) {
+    std::vector<int32_t> tg;
+    if (!copy_back(tg, targets, static_cast<size_t>(num_rows))) return UATTN_EINVAL;
+    for (int32_t t : tg)
+      if (t < 0 || t >= vocab) return UATTN_EINVAL;
+  }
+  uattn::LmHeadLaunch a;
+  a.hidden = hidden;
+  a.hidden_stride = hidden_stride;
+  a.weight = weight;
+  a.weight_stride = weight_stride;
+  a.logits = logits;
+  a.logits_stride = logits != nullptr ? logits_stride : 0;
+  a.num_rows = num_rows;
+  a.vocab = vocab;
+  a.hidden_dim = hidden_dim;
+  return uattn::launch_lm_head_logprob(a, targets, inv_temperature, logp, workspace,
+                                       static_cast<hipStream_t>(stream)) == hipSuccess
+             ? UATTN_OK
+             : UATTN_ELAUNCH;
+}
+
 size_t uattn_prefill_backward_workspace_bytes(int32_t total_tokens, int32_t num_q_heads) {
   if (total_tokens <= 0 || num_q_heads <= 0) return 0;
   return uattn::backward_ws_bytes(total_tokens, num_q_heads);

@@ -100,6 +100,11 @@ struct LmHeadLaunch {
 };
 
 hipError_t launch_lm_head(const LmHeadLaunch& a, hipStream_t stream);
+// LM head with the fused log-probability epilogue (a.logits may be nullptr):
+// partials in `workspace` (lm_head_logprob_ws_bytes), then their fold into logp.
+hipError_t launch_lm_head_logprob(const LmHeadLaunch& a, const int32_t* targets, float inv_temperature, float* logp,
+                                  void* workspace, hipStream_t stream);
+size_t lm_head_logprob_ws_bytes(int64_t num_rows, int64_t vocab);
 
 struct BackwardLaunch {
   const void* q;

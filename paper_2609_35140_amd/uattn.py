@@ -59,6 +59,11 @@ def _load():
     lib.uattn_rope_cache.argtypes = [c_p, c_i32, c_i32, ctypes.c_double, c_p]
     lib.uattn_lm_head.restype = c_i32
     lib.uattn_lm_head.argtypes = [c_p, c_i64, c_p, c_i64, c_i32, c_i32, c_i32, c_p, c_i64, c_p]
+    lib.uattn_lm_head_logprob_workspace_bytes.restype = c_sz
+    lib.uattn_lm_head_logprob_workspace_bytes.argtypes = [c_i32, c_i32]
+    lib.uattn_lm_head_logprob.restype = c_i32
+    lib.uattn_lm_head_logprob.argtypes = [c_p, c_i64, c_p, c_i64, c_p, c_i32, c_i32, c_i32, c_f, c_p, c_p, c_i64, c_p,
+                                          c_sz, c_p]
     lib.uattn_prefill_backward_workspace_bytes.restype = c_sz
     lib.uattn_prefill_backward_workspace_bytes.argtypes = [c_i32, c_i32]
     lib.uattn_prefill_backward.restype = c_i32
@@ -427,6 +432,43 @@ def lm_head(hidden, weight, out=None, stream=None):
     _need(out.dtype == torch.bfloat16 and out.is_cuda and out.shape == (T, V) and out.stride(1) == 1, "out shape")
     _check(_load().uattn_lm_head(_ptr(hidden), hidden.stride(0), _ptr(weight), weight.stride(0), T, V, H, _ptr(out),
                                  out.stride(0), _stream(stream)))
+    return out
+
+
+def lm_head_logprob_workspace_bytes(num_rows: int, vocab: int) -> int:
+    return int(_load().uattn_lm_head_logprob_workspace_bytes(int(num_rows), int(vocab)))
+
+
+def lm_head_logprob(hidden, weight, targets, inv_temperature: float = 1.0, out=None, logits=None, workspace=None,
+                    stream=None):
+    """LM head fused with the token log-probability (uattn_lm_head_logprob).
+
+      hidden [T, H], weight [V, H] bf16 (rows may be strided); targets [T] int32.
+      Returns logp [T] fp32.  ``logits`` ([T, V] bf16, row stride a multiple
+      of 8), when given, also receives the logits.
+    """
+    import torch
+    for name, t in (("hidden", hidden), ("weight", weight)):
+        _need(t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 2 and t.stride(1) == 1,
+              f"{name} must be a 2-D bfloat16 GPU tensor with contiguous rows")
+    T, H = hidden.shape
+    V, H2 = weight.shape
+    _need(H2 == H, "hidden and weight widths differ")
+    _need(targets.dtype == torch.int32 and targets.is_cuda and targets.shape == (T,) and targets.is_contiguous(),
+          "targets must be [T] int32 on the GPU")
+    if out is None:
+        out = torch.empty(T, dtype=torch.float32, device=hidden.device)
+    _need(out.dtype == torch.float32 and out.is_cuda and out.shape == (T,) and out.is_contiguous(), "out must be [T] fp32")
+    if logits is not None:
+        _need(logits.dtype == torch.bfloat16 and logits.is_cuda and logits.shape == (T, V) and logits.stride(1) == 1,
+              "logits must be [T, V] bf16 with contiguous rows")
+    need = lm_head_logprob_workspace_bytes(T, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=hidden.device)  # no initial contents needed
+    _check(_load().uattn_lm_head_logprob(_ptr(hidden), hidden.stride(0), _ptr(weight), weight.stride(0), _ptr(targets),
+                                         T, V, H, float(inv_temperature), _ptr(out), _ptr(logits),
+                                         logits.stride(0) if logits is not None else 0, _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(), _stream(stream)))
     return out
 
 

@@ -236,7 +236,28 @@ def test_ceilings_library_exports_its_header():
         getattr(so, n)
     lib = ceilings.lib()
     # argument checks before any GPU call
-    assert lib.uattn_ceiling_read(P(16), None, 4, 4096, P(16), None) == 1      # block not a multiple of 16 KB
-    assert lib.uattn_ceiling_read(P(18), None, 4, 16384, P(16), None) == 1     # misaligned
-    assert lib.uattn_ceiling_read(P(16), None, 0, 16384, P(16), None) == 0     # nothing to read
+    assert lib.uattn_ceiling_read(P(16), None, 4, 4096, 0, P(16), None) == 1      # block not a multiple of 16 KB
+    assert lib.uattn_ceiling_read(P(18), None, 4, 16384, 0, P(16), None) == 1     # misaligned
+    assert lib.uattn_ceiling_read(P(16), None, 4, 16384, 2, P(16), None) == 1     # unknown flag
+    assert lib.uattn_ceiling_read(P(16), None, 0, 16384, 1, P(16), None) == 0     # nothing to read
     assert lib.uattn_ceiling_mfma(0, 10, P(16), None) == 1
+
+
+def test_lm_head_logprob_workspace_and_argument_checks(lib):
+    from paper_2609_35140_amd import uattn
+    # two fp32 partials per (row, 256-entry vocab tile) plus the target logit per row
+    assert uattn.lm_head_logprob_workspace_bytes(8192, 151936) == (2 * 594 + 1) * 8192 * 4
+    assert uattn.lm_head_logprob_workspace_bytes(3, 256) == 3 * 3 * 4
+    assert uattn.lm_head_logprob_workspace_bytes(0, 100) == 0
+
+    def call(**kw):
+        a = dict(h=P(16), hs=1024, w=P(16), ws=1024, tg=P(16), T=4, V=1000, H=1024, it=1.0, lp=P(16), lg=None,
+                 ls=0, wk=P(16), wkb=1 << 20, stream=None)
+        a.update(kw)
+        return lib.uattn_lm_head_logprob(a["h"], a["hs"], a["w"], a["ws"], a["tg"], a["T"], a["V"], a["H"], a["it"],
+                                         a["lp"], a["lg"], a["ls"], a["wk"], a["wkb"], a["stream"])
+    for kw, code in [(dict(H=100), 1), (dict(hs=512), 1), (dict(it=0.0), 1), (dict(it=float("nan")), 1),
+                     (dict(tg=None), 1), (dict(lp=None), 1), (dict(h=P(18)), 1), (dict(V=0), 1),
+                     (dict(lg=P(16), ls=999), 1), (dict(lg=P(18), ls=1000), 1), (dict(wk=None), 3), (dict(wkb=100), 3),
+                     (dict(wk=P(18)), 3), (dict(T=0), 0), (dict(T=-1), 1)]:
+        assert call(**kw) == code, kw

@@ -287,6 +287,32 @@ def test_workspace_reuse_across_batch_sizes(ua):
         assert int(cnt.abs().sum().item()) == 0, trial
 
 
+def test_workspace_at_a_reused_address_holding_garbage(ua):
+    """A caller's workspace that is not from new_workspace, at a device address
+    an earlier workspace used, holding garbage: the binding zeroes its counter
+    region on first use (it keeps no record keyed by address), so results equal
+    a fresh workspace's every time."""
+    import torch
+    w = inputs.custom(8, 2, 128, [2100, 900, 1500], sigma=0.5, page_size=64)
+    pk = gu.Pack(w, seed=29)
+    ents = [(0, 2099), (1, 899), (2, 1499), (0, 700)]
+    q, t, s, m, _ = pk.decode_rows(ents)
+    ref = ua.decode(q, pk.kp, pk.vp, t, s, m)
+    need = ua.decode_workspace_bytes(len(ents), m, 8, 128)
+    addrs = set()
+    for trial in range(3):
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        addrs.add(ws.data_ptr())
+        ws.fill_(0xA5)                      # garbage where the arrival counters live
+        got = ua.decode(q, pk.kp, pk.vp, t, s, m, workspace=ws)
+        assert torch.equal(got.view(torch.int16), ref.view(torch.int16)), trial
+        got = ua.decode(q, pk.kp, pk.vp, t, s, m, workspace=ws)   # second call on the same tensor
+        assert torch.equal(got.view(torch.int16), ref.view(torch.int16)), trial
+        torch.cuda.synchronize()
+        del ws, got                         # the caching allocator hands the same block out again
+    print(f"workspace addresses seen: {len(addrs)} (1 means every trial reused the freed block)", flush=True)
+
+
 def test_oversized_max_seqlen_gives_the_same_bits(ua):
     """max_seqlen far above every entry's length (a caller passing its
     allocation size): the kernel's walk stops after the longest entry's last

@@ -31,6 +31,8 @@ def test_read_checksum_contiguous_and_paged(cl):
     perm = torch.from_numpy(g.permutation(nblk).astype(np.int32)).cuda()
     ck = cl.read(src, perm, 16384)
     assert int(np.bitwise_xor.reduce(ck.cpu().numpy().view(np.uint32))) == want
+    ck = cl.read(src, perm, 16384, nontemporal=True)
+    assert int(np.bitwise_xor.reduce(ck.cpu().numpy().view(np.uint32))) == want
     # half the blocks, in a random order: the XOR of exactly those blocks
     half = g.permutation(nblk)[: nblk // 2].astype(np.int32)
     ck = cl.read(src, torch.from_numpy(half).cuda(), 16384)

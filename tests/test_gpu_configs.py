@@ -358,3 +358,24 @@ def test_c5_long_context_and_logprob(ua):
     assert err.max() < 2e-5
     del logits, full
     _free()
+
+    # the fused LM head + log-prob at the long-context step's size: 8192 response rows, hidden 8192
+    # (64 q heads x 128), vocabulary 151936, weights ~ N(0, sigma^2 / H); sampled rows against the
+    # oracle's reference and derived bound, and the batch-invariance of the rows
+    H = w.num_q_heads * w.head_dim
+    hidden = inputs.normal_bf16_device((rows, H), 1.0, 7, 1)
+    lm_w = inputs.normal_bf16_device((V, H), w.logit_sigma / float(np.sqrt(H)), 7, 2)
+    tg = torch.from_numpy(inputs.targets(rows, V)).cuda()
+    lp = ua.lm_head_logprob(hidden, lm_w, tg)
+    sample = np.sort(g.choice(rows, size=64, replace=False))
+    si = torch.from_numpy(sample).cuda()
+    one = ua.lm_head_logprob(hidden[si].contiguous(), lm_w, tg[si].contiguous())
+    assert torch.equal(one.view(torch.int32), lp[si].view(torch.int32))
+    ref, bound = oracle.lm_head_logprob_fp64(cfg.host_bits(hidden[si]), cfg.host_bits(lm_w),
+                                             inputs.targets(rows, V)[sample])
+    err = np.abs(lp[si].cpu().numpy().astype(np.float64) - ref)
+    print(f"c5 fused LM head + logprob: 64 sampled rows of {rows}: max err {err.max():.3g}, max err/bound "
+          f"{np.max(err / bound):.3f}; sub-batch bitwise equal", flush=True)
+    assert np.all(err <= bound)
+    del hidden, lm_w, lp
+    _free()
