@@ -47,7 +47,7 @@ extern "C" {
 typedef enum {
   UATTN_OK = 0,
   UATTN_EINVAL = 1,       /* null pointer, negative or inconsistent sizes, Hq % Hkv != 0, bad scale */
-  UATTN_EUNSUPPORTED = 2, /* head_dim not 64/128, page_size not a power of two >= 16, group > 32 */
+  UATTN_EUNSUPPORTED = 2, /* head_dim not 64/128, page_size not a power of two >= 16, group > 32, decode max_seqlen > 2^24 */
   UATTN_EWORKSPACE = 3,   /* decode workspace missing or smaller than uattn_decode_workspace_bytes() */
   UATTN_ELAUNCH = 4,      /* the HIP runtime rejected a kernel launch */
   UATTN_ESCRATCH = 5      /* uattn_decode_noalloc: the sizes need more than UATTN_DECODE_SCRATCH_BYTES */
@@ -113,7 +113,8 @@ size_t uattn_decode_workspace_bytes(int32_t batch, int32_t max_seqlen, int32_t n
  *   seqlens      [batch] int32, 1 <= seqlens[b] <= max_seqlen (includes the
  *                current token); values outside that range are clamped to
  *                it (an entry with seqlens[b] < 1 is left unwritten)
- *   max_seqlen   host int >= every seqlens[b] (sizes grid and workspace only)
+ *   max_seqlen   host int >= every seqlens[b] (sizes grid and workspace only),
+ *                at most 2^24 (UATTN_EUNSUPPORTED above)
  *   out          [batch, num_q_heads, head_dim] bf16 (written)
  *   lse          [batch, num_q_heads] fp32, or NULL
  *   workspace    device scratch of at least

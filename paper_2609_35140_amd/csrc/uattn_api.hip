@@ -128,6 +128,7 @@ uattn_status decode_prepare(const void* q, const void* k_pages, const void* v_pa
   if (page_size < 16 || (page_size & (page_size - 1)) != 0) return UATTN_EUNSUPPORTED;
   if (num_q_heads / num_kv_heads > uattn::kMaxGroup) return UATTN_EUNSUPPORTED;
   if (batch > 65535 || num_kv_heads > 65535) return UATTN_EUNSUPPORTED;
+  if (max_seqlen > (1 << 24)) return UATTN_EUNSUPPORTED;  // keeps every 32-bit workspace offset in range
   if (batch == 0) {
     launch->batch = 0;
     return UATTN_OK;

@@ -38,6 +38,8 @@
 // full-sequence kernel applies at its chunk boundaries.  Chunk boundaries
 // depend only on key positions, so nothing here depends on the batch, its
 // order, the grid, max_seqlen or which workgroup merges.
+#include <type_traits>
+
 #include "uattn_internal.h"
 #include "uattn_numerics.h"
 #include "uattn_tile_io.h"
@@ -74,6 +76,15 @@ __device__ __forceinline__ void st_coherent(float* p, float v) {
 __device__ __forceinline__ float ld_coherent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Buffer access with a wave-uniform base and size: loads at (vector +
+// instruction) offsets past `bytes` return zero without touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), bytes, 0x00020000);
+}
+__device__ __forceinline__ bf16x8 buffer_load16(__amdgpu_buffer_rsrc_t r, int voffset, int soffset) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voffset, soffset, 0));
+}
+
 // 16 bytes per lane with the same device-coherent cache policy (sc1) as the
 // scalar stores above, through a buffer resource: one store instruction per
 // four partial values instead of four, and lanes whose offset lies past the
@@ -85,63 +96,63 @@ __device__ __forceinline__ void st_coherent16(__amdgpu_buffer_rsrc_t r, int voff
 
 // Fold the chunk partials of entry b, kv head kvh (all its q heads) in chunk
 // order and write the normalized outputs.  Called by the workgroup that
-// counted the entry's last outstanding chunk.  Each thread folds two output
-// values and issues the loads of 16 chunks of both before folding, so a
-// context of up to 4096 keys costs one memory round trip.
-template <int D>
+// counted the entry's last outstanding chunk.  A thread folds four
+// consecutive d of one q head (D/4 threads per head, 256 threads cover
+// 4*256/D heads per pass), reading each chunk's four partial values with one
+// 16-byte device-coherent load and the head's (m, l) with one 8-byte load;
+// the loads of kMergeBatch chunks are issued before they are folded, so a
+// pass costs one memory round trip per kMergeBatch chunks.
+template <int D, int kMergeBatch>
 __device__ __forceinline__ void merge_entry(const DecodeParams& p, int b, int kvh, int nch, int tid) {
-  constexpr int kBatch = 16;
-  const int nvals = p.group * D;
-  for (int v0 = tid; v0 < nvals; v0 += 512) {
-    const int vv[2] = {v0, min(v0 + 256, nvals - 1)};
-    const float* ml[2];
-    const float* ac[2];
+  constexpr int kThreadsPerHead = D / 4;
+  constexpr int kHeadsPerPass = 256 / kThreadsPerHead;
+  const int d4 = 4 * (tid % kThreadsPerHead);
+  // resources over the group's partials (wave-uniform); a lane's head and
+  // chunk go into its offset, and offsets past the group read as zero
+  const int64_t slot_g = (static_cast<int64_t>(b) * p.hq + kvh * p.group) * p.nchunk_max;
+  const auto racc = buffer_rsrc(p.ws_acc + slot_g * D, p.group * p.nchunk_max * D * 4);
+  const auto rml = buffer_rsrc(p.ws_ml + slot_g * 2, p.group * p.nchunk_max * 2 * 4);
+  for (int h0 = 0; h0 < p.group; h0 += kHeadsPerPass) {
+    const int gi = h0 + tid / kThreadsPerHead;
+    if (gi >= p.group) break;
+    const int head = kvh * p.group + gi;
+    const int k_base = gi * p.nchunk_max;
+    float M = 0.f, L = 0.f;
+    f32x4 A = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < nch; k0 += kMergeBatch) {
+      f32x4 ba[kMergeBatch];
+      u32x2 bml[kMergeBatch];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int head = kvh * p.group + vv[u] / D;
-      const int64_t base = (static_cast<int64_t>(b) * p.hq + head) * p.nchunk_max;
-      ml[u] = p.ws_ml + base * 2;
-      ac[u] = p.ws_acc + base * D + vv[u] % D;
-    }
-    float M[2] = {0.f, 0.f}, L[2] = {0.f, 0.f}, A[2] = {0.f, 0.f};
-    for (int k0 = 0; k0 < nch; k0 += kBatch) {
-      float bm[2][kBatch], bl[2][kBatch], ba[2][kBatch];
-#pragma unroll
-      for (int i = 0; i < kBatch; ++i) {
-        const int k = min(k0 + i, nch - 1);
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          bm[u][i] = ld_coherent(ml[u] + 2 * k);
-          bl[u][i] = ld_coherent(ml[u] + 2 * k + 1);
-          ba[u][i] = ld_coherent(ac[u] + static_cast<int64_t>(k) * D);
-        }
+      for (int i = 0; i < kMergeBatch; ++i) {
+        // loads of chunks past nch are never folded (past the group's slots they read zero)
+        ba[i] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(racc, ((k_base + k0 + i) * D + d4) * 4, 0, kCoherentPolicy));
+        bml[i] = __builtin_amdgcn_raw_buffer_load_b64(rml, (k_base + k0 + i) * 8, 0, kCoherentPolicy);
       }
 #pragma unroll
-      for (int i = 0; i < kBatch; ++i) {
+      for (int i = 0; i < kMergeBatch; ++i) {
         const int k = k0 + i;
-        if (k >= nch) break;
+        const float m = __uint_as_float(bml[i][0]), l = __uint_as_float(bml[i][1]);
+        if (k == 0) {
+          M = m;
+          L = l;
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          if (k == 0) {
-            M[u] = bm[u][i];
-            L[u] = bl[u][i];
-            A[u] = ba[u][i];
-          } else {
-            const FoldScale f = fold_scale(M[u], bm[u][i], p.c);
-            L[u] = fold_val(f, L[u], bl[u][i]);
-            A[u] = fold_val(f, A[u], ba[u][i]);
-            M[u] = f.m_new;
-          }
+          for (int j = 0; j < 4; ++j) A[j] = ba[i][j];
+        } else if (k < nch) {
+          const FoldScale f = fold_scale(M, m, p.c);
+          L = fold_val(f, L, l);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) A[j] = fold_val(f, A[j], ba[i][j]);
+          M = f.m_new;
         }
       }
     }
+    bf16x4 o;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      if (u == 1 && v0 + 256 >= nvals) break;
-      const int head = kvh * p.group + vv[u] / D, d = vv[u] % D;
-      p.out[(static_cast<int64_t>(b) * p.hq + head) * D + d] = finalize_val(A[u], L[u]);
-      if (p.lse != nullptr && d == 0) p.lse[static_cast<int64_t>(b) * p.hq + head] = finalize_lse(M[u], L[u], p.c);
-    }
+    for (int j = 0; j < 4; ++j) o[j] = finalize_val(A[j], L);
+    const int64_t orow = static_cast<int64_t>(b) * p.hq + head;
+    *reinterpret_cast<bf16x4*>(p.out + orow * D + d4) = o;
+    if (p.lse != nullptr && d4 == 0) p.lse[orow] = finalize_lse(M, L, p.c);
   }
 }
 
@@ -160,14 +171,6 @@ struct DecodeSmem {
   int32_t lenmax[4];                           // per wave: the longest entry it read
 };
 
-// Buffer access with a wave-uniform base and size: loads at (vector +
-// instruction) offsets past `bytes` return zero without touching memory.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), bytes, 0x00020000);
-}
-__device__ __forceinline__ bf16x8 buffer_load16(__amdgpu_buffer_rsrc_t r, int voffset, int soffset) {
-  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voffset, soffset, 0));
-}
 
 // One item as a wave sees it (all fields wave-uniform).
 struct Item {
@@ -251,7 +254,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
   // entry's last outstanding chunk folds them all (always in chunk order).
   // The drain and the barrier make every wave's partial stores complete first.
   int npend = 0;
-  auto drain = [&]() {
+  // kBatch: chunks whose partials a merging thread loads at once (fewer in the
+  // drains inside the walk, where the next item's operands hold registers)
+  auto drain = [&](auto batch_const) {
+    constexpr int kBatch = decltype(batch_const)::value;
     wait_vmem_asm<0>();
     lds_barrier();
     if (tid < npend) {
@@ -264,7 +270,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
     for (int i = 0; i < npend; ++i) {
       if (sm.flag[i]) {
         const int e = sm.pend[i][0];
-        merge_entry<D>(p, e / p.hkv, e % p.hkv, sm.pend[i][1], tid);
+        merge_entry<D, kBatch>(p, e / p.hkv, e % p.hkv, sm.pend[i][1], tid);
         if (tid == 0) __hip_atomic_store(p.ws_cnt + e, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -281,52 +287,66 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
   const int q_off = col * D * 2 + 16 * g;
   const int k_off = row16 * D * 2 + 16 * g;
 
-  Desc desc_next = load_desc(blockIdx.x);
+  // This wave's operands of an item: the group's query rows and the K rows
+  // of its tile, both in the score product's operand registers (query
+  // column col, d = 32*step + 8*g .. +7; key 16*kb + row, the same d), and
+  // where the tile's 16-key blocks live.  Every block is loaded through a
+  // buffer resource sized to its valid bytes, so rows past the context,
+  // blocks on a page outside the pool and tiles or items outside the walk
+  // read as zero without touching memory -- and the number of loads is always
+  // kOpLoads, which the V wait below relies on.
+  constexpr int kOpLoads = (kKeyBlocks + NB) * KS;
+  struct Operands {
+    bf16x8 qf[NB][KS];
+    bf16x8 kf[kKeyBlocks][KS];
+    int64_t boff[kKeyBlocks];  // element offset of key 16*kb of the tile in the pools, -1 if none
+    int rows[kKeyBlocks];      // keys of block kb inside the context
+  };
+  auto issue_ops = [&](const Item& it, const Desc& desc, Operands& op) {
+    const __bf16* qb = p.q + (static_cast<int64_t>(it.b) * p.hq + it.kvh * p.group) * D;
+    const auto rq = buffer_rsrc(qb, it.ntiles > 0 ? p.group * D * 2 : 0);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int st = 0; st < KS; ++st) op.qf[nb][st] = buffer_load16(rq, q_off + nb * kQCols * D * 2 + 64 * st, 0);
+    const int tile = it.chunk * kTilesPerChunk + wave;
+    const bool on = wave < it.ntiles;
+#pragma unroll
+    for (int kb = 0; kb < kKeyBlocks; ++kb) {
+      const int pos = tile * kTileKeys + 16 * kb;
+      const int page = desc.page[kb];
+      const bool ok = on && page >= 0 && page < p.num_pages && pos < it.n;
+      op.rows[kb] = ok ? min(it.n - pos, 16) : 0;
+      op.boff[kb] = ok ? ((static_cast<int64_t>(page) * p.hkv + it.kvh) * p.page_size + (pos & (p.page_size - 1))) * D
+                       : -1;
+      const auto rk = buffer_rsrc(p.kp + (ok ? op.boff[kb] : 0), op.rows[kb] * D * 2);
+#pragma unroll
+      for (int st = 0; st < KS; ++st) op.kf[kb][st] = buffer_load16(rk, k_off + 64 * st, 0);
+    }
+  };
+
+  // Software-pipelined walk: an item's query and K operands are loaded
+  // during the previous item (issued right after that item's V copies), so
+  // every workgroup keeps one item's K rows in flight through the softmax
+  // and PV phases.
+  Desc desc = load_desc(blockIdx.x);
+  Item cur = make_item(blockIdx.x, desc);
+  Desc desc_next = load_desc(min(blockIdx.x + stride, ncand_all - 1));
+  Operands op;
+  issue_ops(cur, desc, op);
 #pragma unroll 1
   for (int item = blockIdx.x; item < ncand; item += stride) {
-    const Desc desc = desc_next;
-    const Item cur = make_item(item, desc);
-    desc_next = load_desc(min(item + stride, ncand_all - 1));
+    const Item next = make_item(item + stride, desc_next);   // empty past the walk
+    const Desc desc_after = load_desc(min(item + 2 * stride, ncand_all - 1));
+    const int tile = cur.chunk * kTilesPerChunk + wave;  // this wave's tile (sequence-relative)
+    const bool tile_on = wave < cur.ntiles;
+
+    // V rows go into LDS slot `wave` by direct-to-LDS loads (16-byte pieces
+    // XOR-swizzled per row), rows past the context from the zero block, so
+    // that V rows meeting zero weights are zero, never stale or NaN.
+    f32x4 s[NB][kKeyBlocks];
     if (cur.ntiles > 0) {
-      const int tile = cur.chunk * kTilesPerChunk + wave;  // this wave's tile (sequence-relative)
-      const bool tile_on = wave < cur.ntiles;
-
-      // Operands.  The query rows of the group and each 16-key block of the
-      // cache are buffer resources sized to their valid bytes, so rows past
-      // the context, or on a page outside the pool, read as zero.  K goes
-      // straight into the score product's A-operand registers (key
-      // 16*kb + row, d = 32*step + 8*g .. +7); V rows go into LDS slot
-      // `wave` by direct-to-LDS loads (16-byte pieces XOR-swizzled per row),
-      // rows past the context from the zero block, so that V rows meeting
-      // zero weights are zero, never stale or NaN.
-      bf16x8 qf[NB][KS], kf[kKeyBlocks][KS];
-      {
-        const __bf16* qb = p.q + (static_cast<int64_t>(cur.b) * p.hq + cur.kvh * p.group) * D;
-        const auto rq = buffer_rsrc(qb, p.group * D * 2);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-          for (int st = 0; st < KS; ++st) qf[nb][st] = buffer_load16(rq, q_off + nb * kQCols * D * 2 + 64 * st, 0);
-      }
-      int64_t boff[kKeyBlocks];  // element offset of key 16*kb of the tile in the pools, -1 if none
-      int rows[kKeyBlocks];      // keys of block kb inside the context
-      if (tile_on) {
-#pragma unroll
-        for (int kb = 0; kb < kKeyBlocks; ++kb) {
-          const int pos = tile * kTileKeys + 16 * kb;
-          const int page = desc.page[kb];
-          const bool ok = page >= 0 && page < p.num_pages && pos < cur.n;
-          rows[kb] = ok ? min(cur.n - pos, 16) : 0;
-          boff[kb] = ok ? ((static_cast<int64_t>(page) * p.hkv + cur.kvh) * p.page_size + (pos & (p.page_size - 1))) * D
-                        : -1;
-          const auto rk = buffer_rsrc(p.kp + (ok ? boff[kb] : 0), rows[kb] * D * 2);
-#pragma unroll
-          for (int st = 0; st < KS; ++st) kf[kb][st] = buffer_load16(rk, k_off + 64 * st, 0);
-        }
-      }
-
       // scores of this wave's tile and their column maxima
-      f32x4 s[NB][kKeyBlocks];
       if (tile_on) {
 #pragma unroll
         for (int kb = 0; kb < kKeyBlocks; ++kb)
@@ -334,7 +354,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
           for (int nb = 0; nb < NB; ++nb) {
             f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int st = 0; st < KS; ++st) a = mfma16(kf[kb][st], qf[nb][st], a);
+            for (int st = 0; st < KS; ++st) a = mfma16(op.kf[kb][st], op.qf[nb][st], a);
             s[nb][kb] = a;
           }
         const int last_tile = (cur.n - 1) / kTileKeys;
@@ -352,11 +372,18 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
           const int slot = i * 64 + lane;
           const int row = slot / TL::kPieces, piece = slot % TL::kPieces;
           const int kb = (i * kRowsPerInstr) / 16;
-          const bool ok = (row & 15) < rows[kb];
-          const __bf16* src = ok ? p.vp + boff[kb] + (row & 15) * D + 8 * (piece ^ TL::v_swz(row)) : zero + 8 * (lane & 15);
+          const bool ok = (row & 15) < op.rows[kb];
+          const __bf16* src =
+              ok ? p.vp + op.boff[kb] + (row & 15) * D + 8 * (piece ^ TL::v_swz(row)) : zero + 8 * (lane & 15);
           dma_b128(src, vbase + i * 64 * 16);
         }
       }
+    }
+    // the next item's operands: exactly kOpLoads loads after this item's V copies
+    Operands op_next;
+    issue_ops(next, desc_next, op_next);
+
+    if (cur.ntiles > 0) {
       lds_barrier();
 
       // running maxima of the chunk's tiles in order, each tile's alpha, and
@@ -383,9 +410,9 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
           sm.pw[wave][nb][1][lane] = pb[1];
         }
       }
-      // this wave's V rows have landed; after the barrier every wave's have
-      wait_barrier<0>();
-
+      // this wave's V rows have landed (only the next item's operand loads
+      // may still be in flight); after the barrier every wave's have
+      wait_barrier<kOpLoads>();
       // PV over the chunk's tiles in ascending order, d blocks NDBW*wave ..
       f32x4 acc[NB][NDBW], lsum[NB];
 #pragma unroll
@@ -449,10 +476,15 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
       // every wave is done with the V tiles, weights and maxima of this item
       lds_barrier();
     }
-    if (npend == SM::kMaxPend) drain();
+    if (npend == SM::kMaxPend) drain(std::integral_constant<int, 8>{});
+    cur = next;
+    op = op_next;
+    desc_next = desc_after;
   }
-  // the end of the walk: count what is pending
-  if (npend > 0) drain();
+  // the end of the walk: count what is pending, and retire the last
+  // (empty) operand prefetch
+  if (npend > 0) drain(std::integral_constant<int, 16>{});
+  wait_vmem_below<0>();
 }
 
 }  // namespace

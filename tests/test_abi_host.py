@@ -97,7 +97,7 @@ def _decode(lib, **kw):
 @pytest.mark.parametrize("kw,code", [
     (dict(hq=9), 1), (dict(page=24), 2), (dict(page=8), 2), (dict(d=80), 2), (dict(hq=66, hkv=2), 2),
     (dict(maxp=3), 1), (dict(maxs=0), 1), (dict(bt=None), 1), (dict(scale=0.0), 1),
-    (dict(npages=0), 1), (dict(npages=-1), 1), (dict(maxs=300, maxp=19), 3), (dict(maxs=300, maxp=19, ws=P(64), wsb=100), 3), (dict(B=0), 0),
+    (dict(npages=0), 1), (dict(npages=-1), 1), (dict(maxs=(1 << 24) + 1, maxp=1 << 20), 2), (dict(maxs=300, maxp=19), 3), (dict(maxs=300, maxp=19, ws=P(64), wsb=100), 3), (dict(B=0), 0),
 ])
 def test_decode_argument_checks(lib, kw, code):
     assert _decode(lib, **kw) == code
