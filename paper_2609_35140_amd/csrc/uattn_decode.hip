@@ -55,10 +55,11 @@ struct DecodeParams {
   const int32_t* seqlens;
   __bf16* out;
   float* lse;
-  float* ws_acc;     // [batch][Hq][nchunk_max][D]
-  float* ws_ml;      // [batch][Hq][nchunk_max][2]
+  float* ws_acc;     // [batch][Hq][nslot][D]
+  float* ws_ml;      // [batch][Hq][nslot][2]
   int32_t* ws_cnt;   // [batch][Hkv] arrival counters, zero between calls
   int batch, hq, hkv, group, maxp, page_size, page_shift, num_pages, max_seqlen, nchunk_max;
+  int nslot;         // partial slots per (entry, q head): nchunk_max rounded up to even
   float c;
 };
 
@@ -99,40 +100,47 @@ __device__ __forceinline__ void st_coherent16(__amdgpu_buffer_rsrc_t r, int voff
 // counted the entry's last outstanding chunk.  A thread folds four
 // consecutive d of one q head (D/4 threads per head, 256 threads cover
 // 4*256/D heads per pass), reading each chunk's four partial values with one
-// 16-byte device-coherent load and the head's (m, l) with one 8-byte load;
-// the loads of kMergeBatch chunks are issued before they are folded, so a
+// 16-byte device-coherent load and the (m, l) pairs of two chunks with one
+// more; the loads of kMergeBatch chunks are issued before they are folded
+// (1.5 * kMergeBatch loads, below the 63 a wave can have outstanding), so a
 // pass costs one memory round trip per kMergeBatch chunks.
 template <int D, int kMergeBatch>
 __device__ __forceinline__ void merge_entry(const DecodeParams& p, int b, int kvh, int nch, int tid) {
+  static_assert(kMergeBatch % 2 == 0 && kMergeBatch * 3 / 2 < 64, "loads in flight");
   constexpr int kThreadsPerHead = D / 4;
   constexpr int kHeadsPerPass = 256 / kThreadsPerHead;
   const int d4 = 4 * (tid % kThreadsPerHead);
   // resources over the group's partials (wave-uniform); a lane's head and
   // chunk go into its offset, and offsets past the group read as zero
-  const int64_t slot_g = (static_cast<int64_t>(b) * p.hq + kvh * p.group) * p.nchunk_max;
-  const auto racc = buffer_rsrc(p.ws_acc + slot_g * D, p.group * p.nchunk_max * D * 4);
-  const auto rml = buffer_rsrc(p.ws_ml + slot_g * 2, p.group * p.nchunk_max * 2 * 4);
+  const int64_t slot_g = (static_cast<int64_t>(b) * p.hq + kvh * p.group) * p.nslot;
+  const auto racc = buffer_rsrc(p.ws_acc + slot_g * D, p.group * p.nslot * D * 4);
+  const auto rml = buffer_rsrc(p.ws_ml + slot_g * 2, p.group * p.nslot * 2 * 4);
   for (int h0 = 0; h0 < p.group; h0 += kHeadsPerPass) {
     const int gi = h0 + tid / kThreadsPerHead;
     if (gi >= p.group) break;
     const int head = kvh * p.group + gi;
-    const int k_base = gi * p.nchunk_max;
+    const int k_base = gi * p.nslot;  // even, so every (m, l) pair load is 16-byte aligned
     float M = 0.f, L = 0.f;
     f32x4 A = {0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < nch; k0 += kMergeBatch) {
       f32x4 ba[kMergeBatch];
-      u32x2 bml[kMergeBatch];
+      f32x4 bml[kMergeBatch / 2];  // (m, l) of chunks k0 + 2i and k0 + 2i + 1
 #pragma unroll
-      for (int i = 0; i < kMergeBatch; ++i) {
+      for (int i = 0; i < kMergeBatch; ++i)
         // loads of chunks past nch are never folded (past the group's slots they read zero)
         ba[i] = __builtin_bit_cast(
             f32x4, __builtin_amdgcn_raw_buffer_load_b128(racc, ((k_base + k0 + i) * D + d4) * 4, 0, kCoherentPolicy));
-        bml[i] = __builtin_amdgcn_raw_buffer_load_b64(rml, (k_base + k0 + i) * 8, 0, kCoherentPolicy);
-      }
+#pragma unroll
+      for (int i = 0; i < kMergeBatch / 2; ++i)
+        bml[i] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(rml, (k_base + k0 + 2 * i) * 8, 0, kCoherentPolicy));
+      // keep the scheduler from sinking the loads into the fold below (they
+      // must all be in flight before the first result is needed)
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < kMergeBatch; ++i) {
         const int k = k0 + i;
-        const float m = __uint_as_float(bml[i][0]), l = __uint_as_float(bml[i][1]);
+        const float m = bml[i / 2][2 * (i % 2)], l = bml[i / 2][2 * (i % 2) + 1];
         if (k == 0) {
           M = m;
           L = l;
@@ -453,16 +461,16 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
       } else {
         // the group's partial rows of this chunk: [head gi][chunk][d], heads
         // past the group fall outside the resource and store nothing
-        const int64_t slot0 = (static_cast<int64_t>(cur.b) * p.hq + cur.kvh * p.group) * p.nchunk_max;
-        const auto racc = buffer_rsrc(p.ws_acc + slot0 * D, p.group * p.nchunk_max * D * 4);
+        const int64_t slot0 = (static_cast<int64_t>(cur.b) * p.hq + cur.kvh * p.group) * p.nslot;
+        const auto racc = buffer_rsrc(p.ws_acc + slot0 * D, p.group * p.nslot * D * 4);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           const int gi = kQCols * nb + col;
-          const int voff = ((gi * p.nchunk_max + cur.chunk) * D + 16 * wave * NDBW + 4 * g) * 4;
+          const int voff = ((gi * p.nslot + cur.chunk) * D + 16 * wave * NDBW + 4 * g) * 4;
 #pragma unroll
           for (int db = 0; db < NDBW; ++db) st_coherent16(racc, voff + 64 * db, acc[nb][db]);
           if (gi < p.group && wave == 0 && g == 0) {
-            const int64_t ws_slot = slot0 + static_cast<int64_t>(gi) * p.nchunk_max + cur.chunk;
+            const int64_t ws_slot = slot0 + static_cast<int64_t>(gi) * p.nslot + cur.chunk;
             st_coherent(p.ws_ml + ws_slot * 2, m_end[nb]);
             st_coherent(p.ws_ml + ws_slot * 2 + 1, lsum[nb][0]);
           }
@@ -483,17 +491,18 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
   }
   // the end of the walk: count what is pending, and retire the last
   // (empty) operand prefetch
-  if (npend > 0) drain(std::integral_constant<int, 16>{});
+  if (npend > 0) drain(std::integral_constant<int, 32>{});
   wait_vmem_below<0>();
 }
 
 }  // namespace
 
-size_t decode_ws_acc_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads, int64_t head_dim) {
-  return (static_cast<size_t>(batch * num_q_heads * nchunk_max * head_dim) * sizeof(float) + 255) / 256 * 256;
+int64_t decode_slots(int64_t nchunk) { return (nchunk + 1) / 2 * 2; }
+size_t decode_ws_acc_bytes(int64_t batch, int64_t nchunk, int64_t num_q_heads, int64_t head_dim) {
+  return (static_cast<size_t>(batch * num_q_heads * decode_slots(nchunk) * head_dim) * sizeof(float) + 255) / 256 * 256;
 }
-size_t decode_ws_ml_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads) {
-  return (static_cast<size_t>(batch * num_q_heads * nchunk_max * 2) * sizeof(float) + 255) / 256 * 256;
+size_t decode_ws_ml_bytes(int64_t batch, int64_t nchunk, int64_t num_q_heads) {
+  return (static_cast<size_t>(batch * num_q_heads * decode_slots(nchunk) * 2) * sizeof(float) + 255) / 256 * 256;
 }
 // Counters are sized by the q-head count (an upper bound of the kv-head count)
 // so that the size depends only on the arguments of uattn_decode_workspace_bytes.
@@ -522,6 +531,7 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
   p.num_pages = a.num_pages;
   p.max_seqlen = a.max_seqlen;
   p.nchunk_max = a.nchunk_max;
+  p.nslot = static_cast<int>(decode_slots(a.nchunk_max));
   p.c = a.c;
   p.batch = a.batch;
   const int64_t ncand = static_cast<int64_t>(a.batch) * a.num_kv_heads * a.nchunk_max;

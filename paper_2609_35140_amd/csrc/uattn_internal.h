@@ -33,8 +33,8 @@ struct DecodeLaunch {
   const int32_t* seqlens;
   void* out;
   float* lse;
-  float* ws_acc;  // [batch][Hq][nchunk_max][head_dim]
-  float* ws_ml;   // [batch][Hq][nchunk_max][2]
+  float* ws_acc;  // [batch][Hq][decode_slots(nchunk_max)][head_dim]
+  float* ws_ml;   // [batch][Hq][decode_slots(nchunk_max)][2]
   int32_t* ws_cnt; // [batch][Hkv] arrival counters
   int32_t batch;
   int32_t max_pages_per_seq;
@@ -146,8 +146,11 @@ uattn_status decode_prepare(const void* q, const void* k_pages, const void* v_pa
 
 // Decode workspace: arrival counters at the start (kept zero between calls),
 // the fp32 partials (acc, then m/l) at the end of the caller's buffer.
-size_t decode_ws_acc_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads, int64_t head_dim);
-size_t decode_ws_ml_bytes(int64_t batch, int64_t nchunk_max, int64_t num_q_heads);
+// Partial slots per (entry, q head) for nchunk chunks: rounded up to even, so
+// that the (m, l) pairs of two consecutive chunks are one 16-byte load.
+int64_t decode_slots(int64_t nchunk);
+size_t decode_ws_acc_bytes(int64_t batch, int64_t nchunk, int64_t num_q_heads, int64_t head_dim);
+size_t decode_ws_ml_bytes(int64_t batch, int64_t nchunk, int64_t num_q_heads);
 size_t decode_ws_cnt_bytes(int64_t batch, int64_t num_q_heads);
 
 }  // namespace uattn

@@ -224,9 +224,9 @@ def counter_bytes(batch: int, num_q_heads: int) -> int:
 def _partials_start(ws_bytes: int, batch: int, max_seqlen: int, num_q_heads: int, head_dim: int) -> int:
     """Byte offset where a call's fp32 partials begin (they sit at the end of
     the workspace; the counters at its start)."""
-    nchunk = (max_seqlen + CHUNK_KEYS - 1) // CHUNK_KEYS
-    acc = (4 * batch * num_q_heads * nchunk * head_dim + 255) // 256 * 256
-    ml = (4 * batch * num_q_heads * nchunk * 2 + 255) // 256 * 256
+    nslot = ((max_seqlen + CHUNK_KEYS - 1) // CHUNK_KEYS + 1) // 2 * 2   # chunks rounded up to even
+    acc = (4 * batch * num_q_heads * nslot * head_dim + 255) // 256 * 256
+    ml = (4 * batch * num_q_heads * nslot * 2 + 255) // 256 * 256
     return (ws_bytes & ~15) - acc - ml
 
 

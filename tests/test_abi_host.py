@@ -61,6 +61,8 @@ def test_workspace_bytes(lib):
     assert uattn.decode_workspace_bytes(8, 257, 32, 128) == _r256(8 * 32 * 4) + 8 * 32 * 2 * 128 * 4 + _r256(8 * 32 * 2 * 2 * 4)
     assert uattn.decode_workspace_bytes(8, 4096, 32, 128) == _r256(8 * 32 * 4) + 8 * 32 * 16 * 128 * 4 + _r256(8 * 32 * 16 * 2 * 4)
     assert uattn.decode_workspace_bytes(3, 300, 5, 64) == _r256(3 * 5 * 4) + _r256(3 * 5 * 2 * 64 * 4) + _r256(3 * 5 * 2 * 2 * 4)
+    # chunk slots rounded up to even: 3 chunks take 4 slots
+    assert uattn.decode_workspace_bytes(2, 600, 8, 128) == _r256(2 * 8 * 4) + 2 * 8 * 4 * 128 * 4 + _r256(2 * 8 * 4 * 2 * 4)
     assert uattn.decode_workspace_bytes(0, 4096, 32, 128) == 0
     assert uattn.decode_workspace_bytes(1, -5, 32, 128) == 0
 
