@@ -273,6 +273,10 @@ __global__ __launch_bounds__(kKvWaves * 64, 1) void bwd_dkdv_kernel(BwdParams p)
   const float c = p.c;
 
   issue(0);
+  // the K/V operands (and stage 0) have landed; the compiler's own wait, so
+  // that it does not keep those register loads pending into the loop, where
+  // its waits would also cover the next stage's loads
+  wait_vmem_below<0>();
   auto step = [&](int it, auto stage_const) {  // step it, in stage SI = it % 2
     constexpr int SI = decltype(stage_const)::value;
     // stage it has landed in every wave, and every wave is done with stage it-1
@@ -460,6 +464,8 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
   const float c = p.c;
 
   issue(0);
+  // the Q/dO operands, D and lse (and stage 0) have landed; see bwd_dkdv_kernel
+  wait_vmem_below<0>();
   auto tile_step = [&](int t, auto stage_const) {  // tile t, in stage SI = t % 2
     constexpr int SI = decltype(stage_const)::value;
     wait_barrier<0>();

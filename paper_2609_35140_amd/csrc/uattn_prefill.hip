@@ -130,6 +130,12 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
 #pragma unroll
   for (int t = 0; t < kStages - 1; ++t)
     if (t <= wg_last_tile) issue_tile(t);
+  // The Q^T operands have landed (and with them the first tiles).  Said with
+  // the compiler's own wait, so that it knows: otherwise it keeps the Q loads
+  // pending through the loop (it cannot see the waits written in assembly)
+  // and waits on the vector-memory count before each tile's first product,
+  // which then also waits for the next tile's loads.
+  wait_vmem_below<0>();
   // tile t, in stage SI = t % kStages, at position POS = t % 4 of its chunk
   auto tile_step = [&](int t, auto stage_const, auto pos_const) {
     constexpr int SI = decltype(stage_const)::value;
