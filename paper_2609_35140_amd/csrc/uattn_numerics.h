@@ -303,6 +303,18 @@ __device__ __forceinline__ FoldScale fold_scale(float M, float m, float c) {
 __device__ __forceinline__ float fold_val(const FoldScale& f, float X, float x) {
   return __builtin_fmaf(f.a, X, f.b * x);
 }
+// The same operation with the result in X's register.  Written as the three-operand
+// v_fma_f32 so that the sum lands in X's register: from fmaf the compiler
+// picks the two-operand form, whose result shares the product's register,
+// and then copies every folded value back (two moves per element of a
+// prefill fold).
+__device__ __forceinline__ float fold_val_tied(const FoldScale& f, float X, float x) {
+  const float bx = f.b * x;
+  float r;
+  // operands: %0 = r (tied to X, %2), %1 = a, %3 = b*x
+  asm("v_fma_f32 %0, %1, %0, %3" : "=v"(r) : "v"(f.a), "0"(X), "v"(bx));
+  return r;
+}
 
 // Final normalization and the optional log-sum-exp (natural log, scaled scores).
 __device__ __forceinline__ __bf16 finalize_val(float A, float L) { return to_bf16(A / L); }

@@ -173,7 +173,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void prefill_kernel(Prefil
 #pragma unroll
             for (int db = 0; db < NDB; ++db)
 #pragma unroll
-              for (int j = 0; j < 4; ++j) A[nb][db][j] = fold_val(f, A[nb][db][j], acc[nb][db][j]);
+              for (int j = 0; j < 4; ++j) A[nb][db][j] = fold_val_tied(f, A[nb][db][j], acc[nb][db][j]);
             M[nb] = f.m_new;
           }
           m[nb] = neg_inf();  // acc and lsum restart at the next chunk's first tile
