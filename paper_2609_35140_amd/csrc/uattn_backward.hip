@@ -492,18 +492,21 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void bwd_dq_kernel(BwdParams p) {
         }
       }
       bf16x8 sb[kDqNB][2];
-      const bool diag = t == my_last_tile;  // wave-uniform: only this tile holds keys after a query
+      // only the diagonal tile holds keys after a query: their scores become
+      // -inf there (a branch on the wave-uniform condition, not a select on
+      // every tile), and exp2 turns them into P = +0, as the forward's mask
+      if (t == my_last_tile) {
+#pragma unroll
+        for (int nb = 0; nb < kDqNB; ++nb) mask_scores(s[nb], t * kTileKeys, q0 + kQCols * nb + col, lane);
+      }
 #pragma unroll
       for (int nb = 0; nb < kDqNB; ++nb) {
-        // key t*64 + 16*kb + 4*g + j is after the query iff 16*kb + j > bound
-        const int bound = q0 + kQCols * nb + col - t * kTileKeys - 4 * g;
         float dsv[4][4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            float x = hw_exp2(__builtin_fmaf(s[nb][kb][j], c, -l2v[nb]));
-            if (diag) x = (score_key(kb, j, 0) > bound) ? 0.f : x;
+            const float x = hw_exp2(__builtin_fmaf(s[nb][kb][j], c, -l2v[nb]));
             dsv[kb][j] = x * (dp[nb][kb][j] - ddv[nb]);
           }
         pack_rows(dsv, sb[nb]);
