@@ -164,19 +164,96 @@ __device__ __forceinline__ void merge_entry(const DecodeParams& p, int b, int kv
   }
 }
 
+// The same fold as merge_entry, in a kernel of its own that runs after a long
+// walk (whose merges would otherwise all fall at its end, one workgroup per
+// (entry, kv head) reading 256-chunk histories alone): here one wave folds 64
+// consecutive d of one (entry, q head) row, so the partials are read by every
+// CU at once.  A lane holds one d; per batch of kMB chunks it issues all their
+// partial loads and lane i loads the (m, l) pair of chunk k0 + i.  The fold
+// scales of the batch are then formed lane-parallel: the running maximum
+// before each chunk is an inclusive scan of the chunk maxima (the IEEE maximum
+// is exact, associative and commutative, so the scan reproduces the left-to-
+// right chain bit for bit), and lane i evaluates fold_scale for chunk k0 + i
+// with exactly the arguments the sequential fold passes.  The fold itself
+// stays sequential in chunk order, taking each chunk's (a, b, l) from its lane.
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams p) {
+  constexpr int kSlices = D / 64;  // waves per row
+  constexpr int kMB = 32;          // chunks per load batch
+  const int lane = threadIdx.x & 63;
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= p.batch * p.hq * kSlices) return;
+  const int row = w / kSlices;  // b * Hq + q head
+  const int d = (w % kSlices) * 64 + lane;
+  const int n = min(p.seqlens[row / p.hq], p.max_seqlen);
+  const int nch = (n + kChunkKeys - 1) / kChunkKeys;
+  if (nch < 2) return;  // a one-chunk entry's output was written by the walk
+  const float* acc = p.ws_acc + static_cast<int64_t>(row) * p.nslot * D + d;
+  const float2* ml = reinterpret_cast<const float2*>(p.ws_ml) + static_cast<int64_t>(row) * p.nslot;
+  float M = 0.f, L = 0.f, A = 0.f;
+  for (int k0 = 0; k0 < nch; k0 += kMB) {
+    const int cnt = min(kMB, nch - k0);
+    float x[kMB];
+#pragma unroll
+    for (int i = 0; i < kMB; ++i) x[i] = i < cnt ? acc[static_cast<int64_t>(k0 + i) * D] : 0.f;
+    const float2 mlv = lane < cnt ? ml[k0 + lane] : make_float2(neg_inf(), 0.f);
+    // running maximum through chunk k0 + lane (lanes past cnt come after
+    // every valid one and change none of their values)
+    float run = mlv.x;
+#pragma unroll
+    for (int sh = 1; sh < 64; sh <<= 1) {
+      const float o = __shfl_up(run, sh, 64);
+      if (lane >= sh) run = vmax(run, o);
+    }
+    if (k0 > 0) run = vmax(M, run);
+    float before = __shfl_up(run, 1, 64);
+    if (lane == 0) before = M;
+    const FoldScale mine = fold_scale(before, mlv.x, p.c);
+#pragma unroll
+    for (int i = 0; i < kMB; ++i) {
+      if (i < cnt) {
+        const float l = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mlv.y), i));
+        if (k0 + i == 0) {
+          L = l;
+          A = x[i];
+        } else {
+          FoldScale f;
+          f.a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mine.a), i));
+          f.b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mine.b), i));
+          L = fold_val(f, L, l);
+          A = fold_val(f, A, x[i]);
+        }
+      }
+    }
+    M = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, run), cnt - 1));
+  }
+  p.out[static_cast<int64_t>(row) * D + d] = finalize_val(A, L);
+  if (p.lse != nullptr && d == 0) p.lse[row] = finalize_lse(M, L, p.c);
+}
+
 constexpr int64_t kLdsBytesPerCu = 160 * 1024;
 constexpr int kLenScanMax = 4096;  // batches up to this size skip chunks past their longest entry
 
-template <int D, int NB>
+// Buffered variant, for long walks: finished partials wait in LDS and go to
+// the workspace in one burst per drain, instead of a few stores per item mixed
+// into the K/V read stream (writes interleaved with a saturated read stream
+// cost far more than their bytes), and decode_merge_kernel folds them after
+// the walk.  Room for 16 items of 8 q heads x 128 d.
+constexpr int kBufFloats = 17152;
+
+template <int D, int NB, bool kBuf>
 struct DecodeSmem {
   using TL = TileLayout<D>;
   static constexpr int kMaxPend = 32;          // finished partials awaiting their arrival count
   __bf16 v[kTilesPerChunk][TL::kTileElems];    // V tile t of the item, TileLayout V swizzle
   bf16x8 pw[kTilesPerChunk][NB][2][64];        // bf16 weights of tile t in each lane's PV operand order
   float tmax[kTilesPerChunk][NB][kQCols];      // column maxima of tile t's scores
-  int32_t pend[kMaxPend][2];                   // (b * Hkv + kv head, chunk count)
+  int32_t pend[kMaxPend][3];                   // (b * Hkv + kv head, chunk count, chunk)
   int32_t flag[kMaxPend];
   int32_t lenmax[4];                           // per wave: the longest entry it read
+  // kBuf: per pending item, G rows of D + 4 floats (acc; the padding spreads
+  // the 16 heads of a store over the banks), then G (m, l) pairs
+  alignas(16) float pbuf[kBuf ? kBufFloats : 4];
 };
 
 
@@ -188,11 +265,11 @@ struct Item {
   int ntiles;  // tiles of this chunk that hold keys (0: nothing to do)
 };
 
-template <int D, int NB>
-__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const int32_t* __restrict__ seqlens,
-                                                        const int32_t* __restrict__ block_table) {
+template <int D, int NB, bool kBuf>
+__global__ __launch_bounds__(256, kBuf ? 1 : 2) void decode_kernel(DecodeParams p, const int32_t* __restrict__ seqlens,
+                                                                   const int32_t* __restrict__ block_table) {
   using TL = TileLayout<D>;
-  using SM = DecodeSmem<D, NB>;
+  using SM = DecodeSmem<D, NB, kBuf>;
   constexpr int KS = D / 32;                   // K steps of the score product
   constexpr int NDBW = D / 16 / 4;             // 16-wide d blocks of the output per wave
   constexpr int kVInstr = TL::kPieces;         // 1 KB direct-to-LDS instructions per V tile
@@ -264,8 +341,42 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
   int npend = 0;
   // kBatch: chunks whose partials a merging thread loads at once (fewer in the
   // drains inside the walk, where the next item's operands hold registers)
+  // buffered partials: one slot per pending item (16-byte aligned)
+  const int item_floats = (p.group * (D + 4) + 2 * p.group + 3) & ~3;
+  const int cap = kBuf ? min(SM::kMaxPend, kBufFloats / item_floats) : SM::kMaxPend;
   auto drain = [&](auto batch_const) {
     constexpr int kBatch = decltype(batch_const)::value;
+    if constexpr (kBuf) {
+      // the pending partials from LDS to their workspace rows, 16 bytes per
+      // thread and step, consecutive threads along a row; plain stores, read
+      // only by the merge kernel that follows, so nothing waits for them
+      lds_barrier();
+      constexpr int kRowPieces = D / 4;
+      const int per_item = p.group * kRowPieces;
+#pragma unroll 1
+      for (int k = tid; k < npend * per_item; k += 256) {
+        const int sl = k / per_item, r = k % per_item;
+        const int gi = r / kRowPieces, pc = r % kRowPieces;
+        const int e = sm.pend[sl][0];
+        const int64_t row =
+            (static_cast<int64_t>(e / p.hkv) * p.hq + (e % p.hkv) * p.group + gi) * p.nslot + sm.pend[sl][2];
+        *reinterpret_cast<f32x4*>(p.ws_acc + row * D + 4 * pc) =
+            *reinterpret_cast<const f32x4*>(sm.pbuf + sl * item_floats + gi * (D + 4) + 4 * pc);
+      }
+#pragma unroll 1
+      for (int k = tid; k < npend * p.group; k += 256) {
+        const int sl = k / p.group, gi = k % p.group;
+        const int e = sm.pend[sl][0];
+        const int64_t row =
+            (static_cast<int64_t>(e / p.hkv) * p.hq + (e % p.hkv) * p.group + gi) * p.nslot + sm.pend[sl][2];
+        *reinterpret_cast<float2*>(p.ws_ml + row * 2) =
+            *reinterpret_cast<const float2*>(sm.pbuf + sl * item_floats + p.group * (D + 4) + 2 * gi);
+      }
+      // every thread's reads of the slots are done before they are refilled
+      lds_barrier();
+      npend = 0;
+      return;
+    }
     wait_vmem_asm<0>();
     lds_barrier();
     if (tid < npend) {
@@ -458,6 +569,28 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
           }
           if (p.lse != nullptr && wave == 0 && g == 0) p.lse[orow] = finalize_lse(m_end[nb], lsum[nb][0], c);
         }
+      } else if constexpr (kBuf) {
+        // this chunk's partial into LDS slot npend (the drain writes it out)
+        float* slotp = sm.pbuf + npend * item_floats;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int gi = kQCols * nb + col;
+          if (gi < p.group) {
+#pragma unroll
+            for (int db = 0; db < NDBW; ++db)
+              *reinterpret_cast<f32x4*>(slotp + gi * (D + 4) + 16 * (wave * NDBW + db) + 4 * g) = acc[nb][db];
+            if (wave == 0 && g == 0) {
+              slotp[p.group * (D + 4) + 2 * gi] = m_end[nb];
+              slotp[p.group * (D + 4) + 2 * gi + 1] = lsum[nb][0];
+            }
+          }
+        }
+        if (tid == 0) {
+          sm.pend[npend][0] = cur.b * p.hkv + cur.kvh;
+          sm.pend[npend][1] = cur.nch;
+          sm.pend[npend][2] = cur.chunk;
+        }
+        ++npend;
       } else {
         // the group's partial rows of this chunk: [head gi][chunk][d], heads
         // past the group fall outside the resource and store nothing
@@ -478,13 +611,14 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeParams p, const in
         if (tid == 0) {
           sm.pend[npend][0] = cur.b * p.hkv + cur.kvh;
           sm.pend[npend][1] = cur.nch;
+          sm.pend[npend][2] = cur.chunk;
         }
         ++npend;
       }
       // every wave is done with the V tiles, weights and maxima of this item
       lds_barrier();
     }
-    if (npend == SM::kMaxPend) drain(std::integral_constant<int, 8>{});
+    if (npend == cap) drain(std::integral_constant<int, 8>{});
     cur = next;
     op = op_next;
     desc_next = desc_after;
@@ -537,6 +671,9 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
   const int64_t ncand = static_cast<int64_t>(a.batch) * a.num_kv_heads * a.nchunk_max;
   if (ncand > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
   const bool two = p.group > kQCols;
+  // long walks (at least 16 items per CU): the buffered variant, one
+  // workgroup per CU
+  const bool buffered = a.nchunk_max > 1 && ncand >= 16 * static_cast<int64_t>(a.num_cus);
   auto launch = [&](auto kernel, size_t smem_bytes) {
     // persistent grid: as many workgroups as the CUs hold at once (LDS-bound)
     const int64_t per_cu = 2 * smem_bytes + 1024 <= kLdsBytesPerCu ? 2 : 1;
@@ -544,16 +681,26 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
     const dim3 grid(static_cast<unsigned>(ncand < slots ? ncand : slots));
     hipLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, p, p.seqlens, p.bt);
   };
+  auto pick = [&](auto d_const, auto nb_const) {
+    constexpr int kD = decltype(d_const)::value, kNB = decltype(nb_const)::value;
+    if (buffered) {
+      launch(decode_kernel<kD, kNB, true>, sizeof(DecodeSmem<kD, kNB, true>));
+      const int64_t waves = static_cast<int64_t>(a.batch) * a.num_q_heads * (kD / 64);
+      hipLaunchKernelGGL(decode_merge_kernel<kD>, dim3(static_cast<unsigned>((waves + 3) / 4)), dim3(256), 0, stream, p);
+    } else {
+      launch(decode_kernel<kD, kNB, false>, sizeof(DecodeSmem<kD, kNB, false>));
+    }
+  };
   if (a.head_dim == 128) {
     if (two)
-      launch(decode_kernel<128, 2>, sizeof(DecodeSmem<128, 2>));
+      pick(std::integral_constant<int, 128>{}, std::integral_constant<int, 2>{});
     else
-      launch(decode_kernel<128, 1>, sizeof(DecodeSmem<128, 1>));
+      pick(std::integral_constant<int, 128>{}, std::integral_constant<int, 1>{});
   } else {
     if (two)
-      launch(decode_kernel<64, 2>, sizeof(DecodeSmem<64, 2>));
+      pick(std::integral_constant<int, 64>{}, std::integral_constant<int, 2>{});
     else
-      launch(decode_kernel<64, 1>, sizeof(DecodeSmem<64, 1>));
+      pick(std::integral_constant<int, 64>{}, std::integral_constant<int, 1>{});
   }
   return hipGetLastError();
 }

@@ -78,6 +78,35 @@ def test_decode_every_position_bitwise_equals_prefill(ua, name, mk, seed):
     assert oracle.parity_report(gu.host_f64(dout), o64)["pass"]
 
 
+@pytest.mark.parametrize("name,mk,seed", SMALL, ids=[s[0] for s in SMALL])
+def test_long_walk_split_merge_bitwise(ua, name, mk, seed):
+    """A walk of at least 16 items per CU (forced here by a max_seqlen far
+    above the lengths) keeps its chunk partials in LDS, writes them in bursts
+    and folds them in a kernel of its own after the walk: every decoded
+    position still equals its prefill row bit for bit, lse included, and the
+    call with the tight max_seqlen."""
+    import torch
+    w = mk()
+    entries = [(s, p) for s, L in enumerate(w.seq_lens) for p in range(L)]
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    nchunk = -(-16 * cus // (len(entries) * w.num_kv_heads)) + 1
+    big = max(256 * nchunk, max(w.seq_lens))
+    page = w.page_size
+    pk = gu.Pack(w, seed=seed, table_slack=-(-big // page))
+    assert pk.table.shape[1] * pk.page >= big
+    assert len(entries) * w.num_kv_heads * (-(-big // 256)) >= 16 * cus
+    out, lse = _prefill(ua, pk)
+    q, table, seqlens, maxs, tok = pk.decode_rows(entries)
+    dout, dlse = ua.decode(q, pk.kp, pk.vp, table, seqlens, big, return_lse=True)
+    eq = gu.rows_equal_bits(gu.host_bits(dout), gu.host_bits(out)[tok])
+    print(name, "long walk bitwise rows", eq.mean(), "max_seqlen", big, flush=True)
+    assert eq.all(), f"{(~eq).sum()} of {eq.size} rows differ"
+    assert np.array_equal(dlse.cpu().numpy().view(np.uint32), lse.cpu().numpy()[tok].view(np.uint32))
+    tight, tight_lse = ua.decode(q, pk.kp, pk.vp, table, seqlens, maxs, return_lse=True)
+    assert torch.equal(tight.view(torch.int16), dout.view(torch.int16))
+    assert torch.equal(tight_lse.view(torch.int32), dlse.view(torch.int32))
+
+
 def test_rising_scores_rescale_path(ua):
     """Keys growing along the sequence make the online softmax's running
     maximum jump inside and across chunks (large rescales and fold factors):
