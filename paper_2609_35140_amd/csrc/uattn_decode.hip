@@ -166,38 +166,87 @@ __device__ __forceinline__ void merge_entry(const DecodeParams& p, int b, int kv
 
 // The same fold as merge_entry, in a kernel of its own that runs after a long
 // walk (whose merges would otherwise all fall at its end, one workgroup per
-// (entry, kv head) reading 256-chunk histories alone): here one wave folds 64
-// consecutive d of one (entry, q head) row, so the partials are read by every
-// CU at once.  A lane holds one d; per batch of kMB chunks it issues all their
-// partial loads and lane i loads the (m, l) pair of chunk k0 + i.  The fold
-// scales of the batch are then formed lane-parallel: the running maximum
-// before each chunk is an inclusive scan of the chunk maxima (the IEEE maximum
-// is exact, associative and commutative, so the scan reproduces the left-to-
-// right chain bit for bit), and lane i evaluates fold_scale for chunk k0 + i
-// with exactly the arguments the sequential fold passes.  The fold itself
-// stays sequential in chunk order, taking each chunk's (a, b, l) from its lane.
+// (entry, kv head) reading 256-chunk histories alone).  A workgroup folds
+// 256 / D consecutive (entry, q head) rows, one d per thread, kMergePass chunks
+// per pass.  Every wave first copies its share of the pass's partials and
+// (m, l) pairs into LDS with direct-to-LDS loads, 1 KB per instruction and the
+// same count in every wave (lanes of chunks past a row's count read the zero
+// block): the (m, l) rows, then the first 64 chunks of every row, then the
+// other 64 -- all in flight at once, which a fold from registers (at most 63
+// loads per wave, each a 256-byte row piece) cannot have.  The first group is
+// folded while the second lands.  Per group of 64 chunks the fold scales are
+// formed lane-parallel: the running maximum before each chunk is an inclusive
+// scan of the chunk maxima (the IEEE maximum is exact, associative and
+// commutative, so the scan reproduces the left-to-right chain bit for bit),
+// and lane i evaluates fold_scale for chunk i of the group with exactly the
+// arguments the sequential fold passes.  The fold itself stays sequential in
+// chunk order, reading each chunk's (a, b, l) back as one broadcast LDS load.
+constexpr int kMergePass = 128;  // chunks per pass: 256 threads x 128 x 4 bytes = 128 KB of LDS
+
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams p) {
-  constexpr int kSlices = D / 64;  // waves per row
-  constexpr int kMB = 32;          // chunks per load batch
-  const int lane = threadIdx.x & 63;
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= p.batch * p.hq * kSlices) return;
-  const int row = w / kSlices;  // b * Hq + q head
-  const int d = (w % kSlices) * 64 + lane;
-  const int n = min(p.seqlens[row / p.hq], p.max_seqlen);
-  const int nch = (n + kChunkKeys - 1) / kChunkKeys;
-  if (nch < 2) return;  // a one-chunk entry's output was written by the walk
-  const float* acc = p.ws_acc + static_cast<int64_t>(row) * p.nslot * D + d;
-  const float2* ml = reinterpret_cast<const float2*>(p.ws_ml) + static_cast<int64_t>(row) * p.nslot;
-  float M = 0.f, L = 0.f, A = 0.f;
-  for (int k0 = 0; k0 < nch; k0 += kMB) {
-    const int cnt = min(kMB, nch - k0);
-    float x[kMB];
+  constexpr int R = 256 / D;                            // rows per workgroup
+  constexpr int kLanesPerChunk = D / 4;                 // 16 bytes per lane
+  constexpr int kChunksPerUnit = 64 / kLanesPerChunk;   // chunks per 1 KB instruction
+  constexpr int kGroupUnits = R * 64 / kChunksPerUnit;  // instructions per group of 64 chunks (all rows)
+  static_assert(kGroupUnits % 4 == 0 && R <= 4, "units split evenly over the waves");
+  constexpr int kUnitsPerWave = kGroupUnits / 4;
+  __shared__ __attribute__((aligned(1024))) float part[R][kMergePass][D];
+  __shared__ __attribute__((aligned(1024))) float2 mlp[R][kMergePass];
+  __shared__ f32x4 scl[4][64];  // per wave: (a, b, l) of the group's chunks
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nrows = p.batch * p.hq;
+  const int row0 = blockIdx.x * R;
+  const char* zero = reinterpret_cast<const char*>(g_zero_rows) + 16 * (lane & 15);
+  // chunk counts of the workgroup's rows (0 past the last row and for
+  // one-chunk entries, whose outputs the walk wrote)
+  int nch_r[R];
+  int nmax = 0;
 #pragma unroll
-    for (int i = 0; i < kMB; ++i) x[i] = i < cnt ? acc[static_cast<int64_t>(k0 + i) * D] : 0.f;
-    const float2 mlv = lane < cnt ? ml[k0 + lane] : make_float2(neg_inf(), 0.f);
-    // running maximum through chunk k0 + lane (lanes past cnt come after
+  for (int r = 0; r < R; ++r) {
+    const int row = row0 + r;
+    const int n = row < nrows ? min(p.seqlens[row / p.hq], p.max_seqlen) : 0;
+    nch_r[r] = (n + kChunkKeys - 1) / kChunkKeys;
+    if (nch_r[r] < 2) nch_r[r] = 0;
+    nmax = max(nmax, nch_r[r]);
+  }
+  // this thread's row (wave-uniform: D >= 64) and d
+  const int my_r = __builtin_amdgcn_readfirstlane(wave * 64 / D);
+  const int d = tid % D;
+  const int row = row0 + my_r;
+  int nch = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    if (r == my_r) nch = nch_r[r];
+  nch = __builtin_amdgcn_readfirstlane(nch);
+
+  // group h of this wave's share of the pass at k0: kUnitsPerWave 1 KB pieces
+  auto issue_group = [&](int k0, int h) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kUnitsPerWave; ++i) {
+      const int u = wave + 4 * i;
+      const int r = u / (64 / kChunksPerUnit);
+      const int kk0 = 64 * h + (u % (64 / kChunksPerUnit)) * kChunksPerUnit;  // wave-uniform
+      const int kk = kk0 + lane / kLanesPerChunk;
+      int nr = 0;
+#pragma unroll
+      for (int rr = 0; rr < R; ++rr)
+        if (rr == r) nr = nch_r[rr];
+      const char* src =
+          k0 + kk < nr ? reinterpret_cast<const char*>(p.ws_acc + (static_cast<int64_t>(row0 + r) * p.nslot + k0 + kk) * D +
+                                                       4 * (lane % kLanesPerChunk))
+                       : zero;
+      dma_b128(src, __builtin_amdgcn_readfirstlane(lds_addr(&part[r][kk0][0])));
+    }
+  };
+  // the sequential fold of chunks kb .. kb + cnt - 1 (kFull: cnt == 64)
+  float M = 0.f, L = 0.f, A = 0.f;
+  auto fold_group = [&](int kb, int cnt, int h, auto full_const) __attribute__((always_inline)) {
+    constexpr bool kFull = decltype(full_const)::value;
+    const float2 mlv = mlp[my_r][64 * h + lane];
+    // running maximum through chunk kb + lane (lanes past cnt come after
     // every valid one and change none of their values)
     float run = mlv.x;
 #pragma unroll
@@ -205,30 +254,77 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams p) {
       const float o = __shfl_up(run, sh, 64);
       if (lane >= sh) run = vmax(run, o);
     }
-    if (k0 > 0) run = vmax(M, run);
+    if (kb > 0) run = vmax(M, run);
     float before = __shfl_up(run, 1, 64);
     if (lane == 0) before = M;
     const FoldScale mine = fold_scale(before, mlv.x, p.c);
+    scl[wave][lane] = f32x4{mine.a, mine.b, mlv.y, 0.f};
 #pragma unroll
-    for (int i = 0; i < kMB; ++i) {
-      if (i < cnt) {
-        const float l = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mlv.y), i));
-        if (k0 + i == 0) {
-          L = l;
-          A = x[i];
-        } else {
-          FoldScale f;
-          f.a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mine.a), i));
-          f.b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, mine.b), i));
-          L = fold_val(f, L, l);
-          A = fold_val(f, A, x[i]);
+    for (int i0 = 0; i0 < 64; i0 += 16) {
+      if (kFull || i0 < cnt) {
+        float x[16];
+        f32x4 f4[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          x[j] = part[my_r][64 * h + i0 + j][d];
+          f4[j] = scl[wave][i0 + j];
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          if (kFull || i0 + j < cnt) {
+            if (kb + i0 + j == 0) {
+              L = f4[j][2];
+              A = x[j];
+            } else {
+              FoldScale f;
+              f.a = f4[j][0];
+              f.b = f4[j][1];
+              L = fold_val(f, L, f4[j][2]);
+              A = fold_val(f, A, x[j]);
+            }
+          }
         }
       }
     }
     M = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, run), cnt - 1));
+  };
+  auto fold = [&](int kb, int h) __attribute__((always_inline)) {
+    if (kb < nch) {
+      const int cnt = min(64, nch - kb);
+      if (cnt == 64)
+        fold_group(kb, 64, h, std::true_type{});
+      else
+        fold_group(kb, cnt, h, std::false_type{});
+    }
+  };
+
+  for (int k0 = 0; k0 < nmax; k0 += kMergePass) {
+    if (wave < R) {
+      // (m, l) of chunks k0 .. k0 + 127 of row `wave`: lane j holds chunks
+      // k0 + 2j and k0 + 2j + 1 (the slot count is even, so both exist)
+      int nr = 0;
+#pragma unroll
+      for (int rr = 0; rr < R; ++rr)
+        if (rr == wave) nr = nch_r[rr];
+      const char* src = k0 + 2 * lane < nr
+                            ? reinterpret_cast<const char*>(p.ws_ml + ((static_cast<int64_t>(row0 + wave) * p.nslot + k0 + 2 * lane) * 2))
+                            : zero;
+      dma_b128(src, __builtin_amdgcn_readfirstlane(lds_addr(&mlp[wave][0])));
+    }
+    issue_group(k0, 0);
+    issue_group(k0, 1);
+    // the (m, l) rows and the first group have landed in every wave
+    wait_barrier<kUnitsPerWave>();
+    fold(k0, 0);
+    wait_barrier<0>();
+    fold(k0 + 64, 1);
+    // every wave is done with this pass's LDS rows before the next fills them
+    lds_barrier();
   }
-  p.out[static_cast<int64_t>(row) * D + d] = finalize_val(A, L);
-  if (p.lse != nullptr && d == 0) p.lse[row] = finalize_lse(M, L, p.c);
+  if (nch >= 2) {
+    p.out[static_cast<int64_t>(row) * D + d] = finalize_val(A, L);
+    if (p.lse != nullptr && d == 0) p.lse[row] = finalize_lse(M, L, p.c);
+  }
 }
 
 constexpr int64_t kLdsBytesPerCu = 160 * 1024;
@@ -685,8 +781,10 @@ hipError_t launch_decode(const DecodeLaunch& a, hipStream_t stream) {
     constexpr int kD = decltype(d_const)::value, kNB = decltype(nb_const)::value;
     if (buffered) {
       launch(decode_kernel<kD, kNB, true>, sizeof(DecodeSmem<kD, kNB, true>));
-      const int64_t waves = static_cast<int64_t>(a.batch) * a.num_q_heads * (kD / 64);
-      hipLaunchKernelGGL(decode_merge_kernel<kD>, dim3(static_cast<unsigned>((waves + 3) / 4)), dim3(256), 0, stream, p);
+      constexpr int kRows = 256 / kD;
+      const int64_t rows = static_cast<int64_t>(a.batch) * a.num_q_heads;
+      hipLaunchKernelGGL(decode_merge_kernel<kD>, dim3(static_cast<unsigned>((rows + kRows - 1) / kRows)), dim3(256), 0,
+                         stream, p);
     } else {
       launch(decode_kernel<kD, kNB, false>, sizeof(DecodeSmem<kD, kNB, false>));
     }
