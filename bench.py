@@ -353,7 +353,8 @@ def main():
                          f"replayed as one HIP graph; HIP events around the phase)"),
         },
         "roofline": {
-            "kernel": "decode_kernel (uattn_decode; split-KV with fused merge)",
+            "kernel": ("uattn_decode = decode_kernel (persistent split-KV walk, partials buffered in LDS) + "
+                       "decode_merge_kernel (chunk-order fold of the partials); a launch is one uattn_decode call"),
             "bound": "hbm",
             "achieved": round(gbs(dec_launch_bytes, dec_launch_ms), 2),
             "peak": HBM_PEAK_GBS,
@@ -364,7 +365,8 @@ def main():
             "traffic_over_algorithmic": round(traffic["hbm_bytes_per_launch"] / dec_launch_bytes, 4) if traffic else None,
             "bytes_per_launch": dec_launch_bytes,
             "avg_launch_ms": round(dec_launch_ms, 5),
-            "avg_launch_ms_is": f"decode-phase event time / {R} launches (includes the graph's inter-launch gaps)",
+            "avg_launch_ms_is": (f"decode-phase event time / {R} uattn_decode calls (both kernels and the graph's "
+                                 f"inter-kernel gaps)"),
         },
         "roofline_prefill": {
             "kernel": f"prefill_kernel (policy-update prefill over {B} x {L})",
