@@ -11,6 +11,7 @@ from .attention import (  # noqa: F401
     CHUNK_KEYS,
     LSE_ABS,
     MAX_ABS,
+    MAX_SLACK,
     MEAN_ABS,
     REL_BF16,
     TILE_KEYS,

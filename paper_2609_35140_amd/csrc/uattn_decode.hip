@@ -12,13 +12,15 @@
 //      maxima in LDS, and only then copies the V rows of tile w into LDS
 //      slot w (direct-to-LDS), so that the K rows meet a memory system
 //      without the V stream;
-//   3. after one barrier every wave forms the running maxima of the chunk's
-//      tiles in order (max is exact, so this is the sequential online-softmax
-//      maximum), wave w turns its tile into bf16 weights against its running
-//      maximum and publishes them in the PV operand order;
+//   3. after one barrier every wave forms the chunk's running reference
+//      maximum through its tiles in order (advance_max on the exact tile
+//      maxima: the sequential online-softmax reference), wave w turns its tile
+//      into bf16 weights against the reference after tile w and publishes them
+//      in the PV operand order;
 //   4. after a second barrier each wave walks the chunk's tiles in ascending
 //      order for a quarter of the output's d range: rescale by that tile's
-//      alpha, then accumulate V^T P^T, exactly the full-sequence sequence.
+//      alpha (skipped when it is 1 in every lane), then accumulate V^T P^T,
+//      exactly the full-sequence sequence.
 //
 // So every element sees the same operations, in the same order, as in the
 // full-sequence kernel, with two barriers per chunk.  An item's result is
@@ -601,8 +603,8 @@ __global__ __launch_bounds__(256, kBuf ? 1 : 2) void decode_kernel(DecodeParams 
     if (cur.ntiles > 0) {
       lds_barrier();
 
-      // running maxima of the chunk's tiles in order, each tile's alpha, and
-      // this wave's weights against its tile's running maximum
+      // the chunk's running reference through its tiles in order, each
+      // tile's alpha, and this wave's weights against its tile's reference
       float alpha[kTilesPerChunk][NB], m_end[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
@@ -610,10 +612,8 @@ __global__ __launch_bounds__(256, kBuf ? 1 : 2) void decode_kernel(DecodeParams 
 #pragma unroll
         for (int t = 0; t < kTilesPerChunk; ++t) {
           if (t < cur.ntiles) {
-            const float m_new = vmax(m, sm.tmax[t][nb][col]);
-            alpha[t][nb] = rescale_alpha(m, m_new, c);
-            if (t == wave) m_mine = m_new;
-            m = m_new;
+            alpha[t][nb] = advance_max(m, sm.tmax[t][nb][col], c);
+            if (t == wave) m_mine = m;
           }
         }
         m_end[nb] = m;

@@ -24,13 +24,20 @@
 //   * the mask is a select to -inf (keys after the query), never a bias;
 //   * softmax runs on raw scores with the scale folded into the exponent:
 //     p = exp2(fma(s, c, -m*c)) with c = fp32(scale * log2(e)) computed once
-//     on the host; alpha = exp2(m_old*c - m_new*c); the hardware v_exp_f32;
+//     on the host; the hardware v_exp_f32;
+//   * the running maximum m of a chunk is a reference that moves to a tile's
+//     maximum t only when t*c - m*c > kMaxSlack (8; always when m = -inf),
+//     with alpha = exp2(m_old*c - t*c); otherwise m stays and alpha is 1, so
+//     weights may reach 2^8 (within fp32 and bf16 range, and every weight
+//     still carries one bf16 rounding of relative size <= 2^-9);
 //   * p is rounded to bf16 (nearest-even) for the PV product, and l is the
 //     sum of the same bf16 p, accumulated by that product (an extra all-ones
 //     row block); acc and l are rescaled by alpha BEFORE the product
 //     accumulates into them;
-//   * no data-dependent skip of any multiply (alpha == 1 included);
-//     subnormals are preserved (the kernels' default fp32 denormal mode);
+//   * the alpha multiplies are skipped only when alpha is exactly 1 in every
+//     lane of the wave (x * 1 == x, so the bits do not depend on which rows
+//     share a wave); no other data-dependent skip; subnormals are preserved
+//     (the kernels' default fp32 denormal mode);
 //   * the result is bf16_rne(A / L) with IEEE division.
 //
 // Floating-point contraction is disabled for everything in this header so
@@ -170,11 +177,21 @@ __device__ __forceinline__ float max_xor16(float x) {
 // every kernel composes in the same order:
 //   tile_max      the column maximum of the (masked) raw scores of the tile,
 //                 in every lane of the column;
-//   rescale_alpha alpha = exp2(m_old*c - m_new*c) with m_new = max(m_old, tile max);
+//   advance_max   the reference after the tile (moves to the tile maximum
+//                 only past the slack) and its alpha;
 //   tile_weights  s <- p = exp2(fma(s, c, -m_new*c)).
 // The row sum l is accumulated by the PV product (pv_tile), from the same
 // bf16 p that weights V.
+//
+// The slack keeps the reference (and with it every accumulator) in place for
+// all but the rare tile whose scores rise more than 2^8 above it in the exp2
+// domain, so the multiplies by alpha -- a quarter of the vector work of a
+// tile -- are almost always skipped; the decode walks the same tiles in the
+// same order through the same function, so both paths keep the same
+// reference.  The fold of chunk partials (fold_scale below) keeps the exact
+// running maximum.
 // ---------------------------------------------------------------------------
+constexpr float kMaxSlack = 8.0f;
 __device__ __forceinline__ float tile_max(const f32x4 (&s)[4]) {
   float t[4];
 #pragma unroll
@@ -183,10 +200,14 @@ __device__ __forceinline__ float tile_max(const f32x4 (&s)[4]) {
   tmax = max_xor16(tmax);
   return max_xor32(tmax);
 }
-__device__ __forceinline__ float rescale_alpha(float m_old, float m_new, float c) {
-  const float mc_old = m_old * c;
-  const float mc_new = m_new * c;
-  return hw_exp2(mc_old - mc_new);
+// m <- the reference after a tile whose maximum is tmax; returns alpha.
+__device__ __forceinline__ float advance_max(float& m, float tmax, float c) {
+  const float mc_old = m * c;
+  const float tc = tmax * c;
+  const bool move = tc - mc_old > kMaxSlack;  // -inf reference: +inf > slack
+  const float alpha = move ? hw_exp2(mc_old - tc) : 1.0f;
+  m = move ? tmax : m;
+  return alpha;
 }
 __device__ __forceinline__ void tile_weights(f32x4 (&s)[4], float m_new, float c) {
   const float mc_new = m_new * c;
@@ -195,13 +216,36 @@ __device__ __forceinline__ void tile_weights(f32x4 (&s)[4], float m_new, float c
 #pragma unroll
     for (int j = 0; j < 4; ++j) s[kb][j] = hw_exp2(__builtin_fmaf(s[kb][j], c, -mc_new));
 }
-// The whole step: s <- p, m <- m_new; returns alpha.
+// The whole step: m <- the new reference, s <- p; returns alpha.
 __device__ __forceinline__ float softmax_tile(f32x4 (&s)[4], float& m, float c) {
-  const float m_new = vmax(m, tile_max(s));
-  const float alpha = rescale_alpha(m, m_new, c);
-  tile_weights(s, m_new, c);
-  m = m_new;
+  const float alpha = advance_max(m, tile_max(s), c);
+  tile_weights(s, m, c);
   return alpha;
+}
+
+// True when some lane of the wave has an alpha other than 1 (the multiplies
+// by alpha are then issued for every lane; x * 1 == x in the others).
+template <int NB>
+__device__ __forceinline__ bool any_rescale(const float (&alpha)[NB]) {
+  bool r = false;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) r = r || alpha[nb] != 1.0f;
+  return __builtin_amdgcn_ballot_w64(r) != 0;
+}
+// acc <- alpha * acc, lsum <- alpha * lsum for the wave's query columns,
+// skipped when every alpha is 1.
+template <int NB, int NDB>
+__device__ __forceinline__ void rescale_acc(f32x4 (&acc)[NB][NDB], f32x4 (&lsum)[NB], const float (&alpha)[NB]) {
+  if (!any_rescale<NB>(alpha)) return;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) lsum[nb][j] = alpha[nb] * lsum[nb][j];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[nb][db][j] = alpha[nb] * acc[nb][db][j];
+  }
 }
 
 // p (fp32, score layout) -> bf16 PV B operand.  Step st covers keys
@@ -222,7 +266,8 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
 }
 
 // acc[nb][db] (O^T block: rows d = 16*(db0+db) + 4*g + j, column = query of nb)
-//   <- alpha[nb] * acc + V^T_db P_nb^T, K steps st = 0, 1 in order;
+//   <- alpha[nb] * acc + V^T_db P_nb^T, K steps st = 0, 1 in order (the
+//   multiplies by alpha through rescale_acc, all before the first product);
 // lsum[nb] <- alpha[nb] * lsum + 1^T P_nb^T: the same product with an all-ones
 // operand in place of V^T, so every register of lsum holds the column's
 // running sum of the bf16 weights (l).
@@ -248,14 +293,10 @@ __device__ __forceinline__ void pv_tile(const __bf16* vtile, const bf16x8 (&pb)[
   bf16x8 ones;
 #pragma unroll
   for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
+  if constexpr (!kFirst) rescale_acc<NB, NDB>(acc, lsum, alpha);
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    if constexpr (kFirst) {
-      lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) lsum[nb][j] = alpha[nb] * lsum[nb][j];
-    }
+    if constexpr (kFirst) lsum[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < 2; ++st) lsum[nb] = mfma16(ones, pb[nb][st], lsum[nb]);
   }
@@ -272,12 +313,7 @@ __device__ __forceinline__ void pv_tile(const __bf16* vtile, const bf16x8 (&pb)[
     }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      if constexpr (kFirst) {
-        acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[nb][db][j] = alpha[nb] * acc[nb][db][j];
-      }
+      if constexpr (kFirst) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < 2; ++st) acc[nb][db] = mfma16(a[st], pb[nb][st], acc[nb][db]);
     }

@@ -116,12 +116,12 @@ def test_emulator_planted_mistakes_fail_gate(monkeypatch):
     o64, _ = oracle.causal_attention_fp64(t["q"], t["k"], t["v"], t["cu_seqlens"])
     real = oa._emulate_rows
 
-    def _last_chunk_only(qh, kh, vh, qpos, c, bn, chunk):
+    def _last_chunk_only(qh, kh, vh, qpos, c, bn, chunk, slack=oa.MAX_SLACK):
         o = np.zeros((qh.shape[0], qh.shape[1]), dtype=np.float32)
         l = np.zeros(qh.shape[0], dtype=np.float32)
         for r in range(qh.shape[0]):
             start = (qpos[r] // chunk) * chunk
-            oo, ll = real(qh[r:r + 1], kh[start:], vh[start:], np.array([qpos[r] - start]), c, bn, chunk)
+            oo, ll = real(qh[r:r + 1], kh[start:], vh[start:], np.array([qpos[r] - start]), c, bn, chunk, slack)
             o[r], l[r] = oo[0], ll[0]
         return o, l
     # keep only the last chunk's partial: a dropped fold term
@@ -160,6 +160,40 @@ def test_emulator_rising_scores_move_the_reference_within_gate():
     assert rep["pass"], rep
     assert np.max(np.abs(lse32 - lse64)) < oracle.LSE_ABS
 
+
+
+@pytest.mark.parametrize("sigma,ramp", [(1.0, 0.0), (0.5, 16.0)])
+def test_emulator_reference_slack_changes_bits_only_within_tolerance(sigma, ramp):
+    """The slack rule (the chunk's reference maximum moves only past a rise of
+    2^8) and the textbook rule (it moves on every rise, slack 0) are the same
+    mathematics: both emulations meet the gate against the fp64 definition,
+    lse included, and they differ from each other only within it.  With the
+    ramped keys the reference moves inside chunks under both rules."""
+    w = inputs.custom(2, 1, 64, [700, 130], sigma=sigma)
+    t = inputs.packed_qkv(w, seed=11)
+    if ramp:
+        t = inputs.ramp_keys(t, ramp)
+    o64, lse64 = oracle.causal_attention_fp64(t["q"], t["k"], t["v"], t["cu_seqlens"])
+    outs = {}
+    for slack in (0.0, oa.MAX_SLACK):
+        o32, lse32 = oracle.tile_emulate_fp32(t["q"], t["k"], t["v"], t["cu_seqlens"], slack=slack)
+        rep = oracle.parity_report(o32, o64)
+        assert rep["pass"], (slack, rep)
+        assert np.max(np.abs(lse32 - lse64)) < oracle.LSE_ABS
+        outs[slack] = (o32, lse32)
+    d = np.abs(outs[0.0][0].astype(np.float64) - outs[oa.MAX_SLACK][0].astype(np.float64))
+    assert np.all(d <= 2 * (oracle.MAX_ABS + oracle.REL_BF16 * np.abs(o64)))
+    assert np.max(np.abs(outs[0.0][1] - outs[oa.MAX_SLACK][1])) < 2 * oracle.LSE_ABS
+
+
+def test_emulator_slack_rule_is_exact_on_one_key_rows():
+    """A first tile moves the reference from -inf under any slack: a row whose
+    context is a single key returns that key's V exactly either way."""
+    w = inputs.custom(2, 1, 64, [1, 1, 1], sigma=1.0)
+    t = inputs.packed_qkv(w, seed=2)
+    for slack in (0.0, oa.MAX_SLACK, 100.0):
+        o32, _ = oracle.tile_emulate_fp32(t["q"], t["k"], t["v"], t["cu_seqlens"], slack=slack)
+        assert np.array_equal(o32[:, 0].astype(np.float64), oracle.bf16_to_f64(t["v"])[:, 0])
 
 
 def test_emulator_one_head_rows_equal_pack_rows():
