@@ -102,6 +102,15 @@ __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 __device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 
 __device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+// The same v_exp_f32 for a value that inline asm reads.  A VALU instruction
+// that reads a transcendental result needs one wait state after it; the
+// compiler adds it only between instructions it generated itself, not before
+// an asm operand, so the asm here carries its own.
+__device__ __forceinline__ float hw_exp2_for_asm(float x) {
+  float r;
+  asm("v_exp_f32 %0, %1\n\ts_nop 0" : "=v"(r) : "v"(x));
+  return r;
+}
 __device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }
 
 __device__ __forceinline__ __bf16 to_bf16(float x) { return static_cast<__bf16>(x); }
@@ -331,7 +340,7 @@ __device__ __forceinline__ FoldScale fold_scale(float M, float m, float c) {
   FoldScale f;
   f.m_new = vmax(M, m);
   const float mc_new = f.m_new * c;
-  f.a = hw_exp2(M * c - mc_new);
+  f.a = hw_exp2_for_asm(M * c - mc_new);  // read by fold_val_tied's asm
   f.b = hw_exp2(m * c - mc_new);
   return f;
 }
