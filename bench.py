@@ -444,7 +444,7 @@ def secondary(torch, np, inputs, uattn):
     steps = uattn.DecodeSteps(q_steps, pk.kp, pk.vp, pk.table_dev, sl, L, out_steps)
     graph = decode_graph(torch, steps, R)
     out_full = torch.empty_like(pk.q)
-    pre_ms = timed(torch, lambda: uattn.prefill(pk.q, pk.k, pk.v, pk.cu_dev, L, out=out_full), 5)
+    pre_ms = timed(torch, lambda: uattn.prefill(pk.q, pk.k, pk.v, pk.cu_dev, L, out=out_full), 20)
     dec_ms = timed(torch, graph.replay, 5)
     eq = (out_steps.view(torch.int16).reshape(R * B, hq, d) == out_full.view(torch.int16)[tok.reshape(-1)]).all(-1)
     dec_bytes = w.decode_kv_bytes()
