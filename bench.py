@@ -147,7 +147,7 @@ def decode_graph(torch, steps, n):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: every GPU box here has one, and the library has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(prefill and decode would shard by sequence or kv head with no exchange). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
